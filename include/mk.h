@@ -1,0 +1,216 @@
+/*
+ * mk.h -- C ABI of libmk: composed multi-operator modules on MI355X (gfx950).
+ *
+ * MKEvolve (arXiv 2607.20501) states the problem as a PyTorch module M,
+ * decomposed into subproblems that a top-level module S chains; each
+ * subproblem has its own, independently verified and swappable, kernel
+ * (Sec. 3, Alg. 1 and "LLMDecompose agent"; App. H.1 shows such an S).  This
+ * library is that hot path: a module is an operator sequence with shapes
+ * (mk_module_desc), a decomposition is a contiguous grouping of its ops
+ * (group_of_op), every group runs as one subkernel made of hand-written HIP
+ * kernels, and each subkernel's implementation can be swapped on its own
+ * (Sec. 3, "Swap").  mk_run executes the composition; mk_verify checks each
+ * materialised stage and the output against caller-given reference values
+ * (Sec. 3 "Evaluate"; App. D, decomposed per-stage checking).
+ *
+ * Conventions
+ *  - Every function returns mk_status; nothing throws across the ABI.  On an
+ *    error, mk_last_error() gives a thread-local message.
+ *  - Tensors are dense and row-major.  Every module input, materialised
+ *    intermediate and the output are stored in the module dtype (float32, or
+ *    bfloat16 as raw 16-bit patterns); arithmetic inside kernels is fp32.
+ *  - Value ids: 0..n_inputs-1 are the module inputs (activations and weights
+ *    alike); n_inputs+i is the output of op i; the module output is the
+ *    output of the last op.
+ *  - Device buffers (inputs, output, workspace) are allocated and owned by the
+ *    caller.  A module owns host-side plan state only; mk_run never allocates
+ *    device memory.  Two concurrent runs of one module need distinct
+ *    workspaces.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ */
+#ifndef MK_H
+#define MK_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MK_OK = 0,
+  MK_E_INVALID_ARG = 1,  /* null pointer, bad id, bad enum value */
+  MK_E_SHAPE = 2,        /* shapes of an op's operands do not agree */
+  MK_E_DTYPE = 3,        /* unknown dtype */
+  MK_E_DECOMP = 4,       /* grouping not contiguous, hides a value another
+                            group reads, or matches no subkernel family */
+  MK_E_UNSUPPORTED = 5,  /* valid request with no implementation (impl id) */
+  MK_E_WORKSPACE = 6,    /* workspace smaller than mk_workspace_size */
+  MK_E_HIP = 7,          /* a HIP runtime call failed; see mk_last_error */
+  MK_E_INTERNAL = 8
+} mk_status;
+
+typedef enum { MK_F32 = 0, MK_BF16 = 1 } mk_dtype;
+
+/* Operators.  Semantics (all over the last dimension unless stated):
+ *  GEMM         in {A[..,K], W}; ip[0] = 0: W is [N,K] and y = A W^T (nn.Linear
+ *               layout), 1: W is [K,N] and y = A W.  y[..,N].
+ *  BIAS         in {x[..,N], b[N]}: x + b.
+ *  BIAS_CHANNEL in {x[N,C,H,W], b[C]}: x + b[c].
+ *  RELU, GELU_ERF (0.5x(1+erf(x/sqrt2))), GELU_TANH
+ *               (0.5x(1+tanh(sqrt(2/pi)(x+0.044715x^3)))), SCALE (x*fp[0]).
+ *  ADD          in {x, r} of equal shape: x + r (residual).
+ *  ROWSUM       [..,N] -> [..]: sum over the last dimension.
+ *  SOFTMAX      exp(x - max) / sum over the last dimension.
+ *  LAYERNORM    in {x[..,D], gamma[D], beta[D]}, fp[0] = eps:
+ *               (x - mean) / sqrt(biased var + eps) * gamma + beta.
+ *  CONV2D       in {x[N,C,H,W], w[K,C,R,S]}, ip = {stride, pad}:
+ *               cross-correlation with zero padding -> [N,K,P,Q].
+ *  GAP          [N,C,H,W] -> [N,C]: mean over H*W.
+ *  QK           in {qkv[B*S, 3*H*dh]} packed per token as [Q | K | V], head h
+ *               at columns h*dh..h*dh+dh-1 of each block; ip = {B, H, dh, S};
+ *               fp[0] = scale: s[b,h,i,j] = (q_i . k_j) * scale -> [B,H,S,S].
+ *  CAUSAL_MASK  [..,S,S]: entries with j > i become -inf (diagonal kept).
+ *  PV           in {p[B,H,S,S], qkv}, ip = {B, H, dh, S}:
+ *               o[b,i,h*dh+e] = sum_j p[b,h,i,j] v[b,j,h,e] -> [B,S,H*dh]. */
+typedef enum {
+  MK_OP_GEMM = 0, MK_OP_BIAS, MK_OP_BIAS_CHANNEL, MK_OP_RELU, MK_OP_GELU_ERF,
+  MK_OP_GELU_TANH, MK_OP_SCALE, MK_OP_ADD, MK_OP_ROWSUM, MK_OP_SOFTMAX,
+  MK_OP_LAYERNORM, MK_OP_CONV2D, MK_OP_GAP, MK_OP_QK, MK_OP_CAUSAL_MASK, MK_OP_PV,
+  MK_OP_COUNT
+} mk_op_kind;
+
+typedef struct { int32_t ndim; int64_t dims[4]; } mk_shape;
+
+typedef struct {
+  int32_t kind;     /* mk_op_kind */
+  int32_t in[3];    /* value ids; -1 where unused */
+  int64_t ip[4];    /* integer parameters, see mk_op_kind */
+  double fp[2];     /* real parameters, see mk_op_kind */
+} mk_op;
+
+typedef struct {
+  int32_t dtype;                 /* mk_dtype */
+  int32_t n_inputs;
+  const mk_shape* input_shapes;  /* [n_inputs] */
+  int32_t n_ops;                 /* 1..64 */
+  const mk_op* ops;              /* [n_ops] */
+} mk_module_desc;
+
+typedef struct mk_module mk_module;
+
+/* Subkernel families (what a group of ops is run as). */
+typedef enum {
+  MK_FAM_GEMM = 0,   /* [LAYERNORM] GEMM|QK|PV, element-wise epilogue, [ROWSUM|SOFTMAX] */
+  MK_FAM_CONV = 1,   /* CONV2D, element-wise epilogue, [GAP] */
+  MK_FAM_EW = 2,     /* chain of element-wise ops */
+  MK_FAM_ROW = 3,    /* element-wise prologue, then ROWSUM|SOFTMAX|LAYERNORM|GAP */
+  MK_FAM_ATTN = 4    /* QK [CAUSAL_MASK] SOFTMAX PV */
+} mk_family;
+
+/* Implementation ids accepted by mk_subkernel_select. */
+enum { MK_IMPL_TUNED = 0, MK_IMPL_SIMPLE = 1, MK_IMPL_MUTANT_BASE = 100 };
+
+typedef struct {
+  int32_t n_subkernels;
+  int32_t n_ops;
+  mk_shape out_shape;
+  int64_t ws_bytes;               /* workspace mk_run needs (intermediates + scratch) */
+  int64_t ws_intermediate_bytes;  /* sum of round_up(bytes, 256) of materialised intermediates */
+  int64_t flops;                  /* algorithmic flops of the module */
+  int64_t alg_bytes;              /* module inputs read once + output written once */
+} mk_module_info_t;
+
+typedef struct {
+  int32_t op_begin, op_end;       /* ops [begin, end) */
+  int32_t out_value;              /* value id of the materialised output */
+  mk_shape out_shape;
+  int64_t out_bytes;
+  int64_t ws_offset;              /* byte offset in the workspace; -1 = module output buffer */
+  int64_t flops;                  /* algorithmic flops of the group's ops */
+  int64_t alg_bytes;              /* distinct external inputs read once + output written once */
+  int32_t family;                 /* mk_family */
+  int32_t impl;                   /* selected implementation id */
+  int32_t n_launches;             /* kernel launches of the selected implementation */
+  int64_t scratch_bytes;          /* scratch the selected implementation uses */
+} mk_subkernel_info_t;
+
+/* Fill group_of_op[n_ops] with a preset decomposition.  preset 0 = split (one
+ * subkernel per op, except that a BIAS, BIAS_CHANNEL or ADD joins the GEMM or
+ * CONV2D that produces its input); preset 1 = fused (from each op, the longest
+ * group a family accepts).  Host only. */
+mk_status mk_decomposition_preset(const mk_module_desc* desc, int32_t preset,
+                                  int32_t* group_of_op);
+
+/* Validate the module (shape inference) and the grouping, match every group to
+ * a family and lay out the workspace.  Host only: no device is touched.
+ * group_of_op[i] is op i's group; groups are numbered 0,1,.. in op order.
+ * On success *out owns a new module (free with mk_module_destroy). */
+mk_status mk_module_create(const mk_module_desc* desc, const int32_t* group_of_op,
+                           mk_module** out);
+void mk_module_destroy(mk_module* m);
+
+mk_status mk_module_info(const mk_module* m, mk_module_info_t* info);
+mk_status mk_subkernel_info(const mk_module* m, int32_t i, mk_subkernel_info_t* info);
+
+/* Swap subkernel i's implementation (MK_IMPL_TUNED, MK_IMPL_SIMPLE or a
+ * test-only mutant id).  MK_E_UNSUPPORTED if the family has no such impl. */
+mk_status mk_subkernel_select(mk_module* m, int32_t i, int32_t impl_id);
+
+mk_status mk_workspace_size(const mk_module* m, int64_t* bytes);
+
+/* Enqueue the composition on `stream`.  dev_inputs[n_inputs] are device
+ * pointers to the module inputs, dev_out receives the module output, dev_ws is
+ * a device workspace of ws_bytes >= mk_workspace_size.  Returns after
+ * enqueueing, unless per_subkernel_ms is non-NULL: then each subkernel is
+ * bracketed by HIP events, the stream is synchronised and per_subkernel_ms[i]
+ * receives subkernel i's elapsed milliseconds. */
+mk_status mk_run(mk_module* m, const void* const* dev_inputs, void* dev_out, void* dev_ws,
+                 int64_t ws_bytes, void* stream, float* per_subkernel_ms);
+
+/* One reference check: stage s is subkernel s's materialised output (the last
+ * subkernel's is the module output).  Element index[k] (flat, row-major; NULL
+ * means index k) of that tensor must satisfy
+ *   |got - expect[k]| <= atol + rtol * |expect[k]|
+ * (the torch.allclose criterion, App. D); an infinite expect must be matched
+ * exactly and a non-finite got against a finite expect always fails. */
+typedef struct {
+  int32_t stage;
+  int64_t n;
+  const int64_t* index;   /* host, [n] or NULL */
+  const double* expect;   /* host, [n] */
+  double rtol, atol;
+} mk_check;
+
+typedef struct {
+  int32_t stage;
+  int32_t pass;
+  int64_t n_checked, n_violations, n_nonfinite;
+  double max_abs_err, max_rel_err;
+  double worst_ratio;     /* max |err| / (atol + rtol |expect|) */
+  int64_t worst_index;    /* flat index at worst_ratio */
+  double got_at_worst, expect_at_worst;
+} mk_check_result;
+
+enum { MK_MAX_CHECKS = 64 };
+
+typedef struct {
+  int32_t pass;                  /* every check passed */
+  int32_t first_failing_stage;   /* lowest failing stage, -1 if none */
+  int32_t n_results;
+  mk_check_result results[MK_MAX_CHECKS];
+} mk_verify_report;
+
+/* Poison the workspace with NaN bytes, run the module once (as mk_run),
+ * synchronise, copy each checked stage to the host and compare.  Returns MK_OK
+ * when the checks ran; pass/fail is in *report.  n_checks <= MK_MAX_CHECKS. */
+mk_status mk_verify(mk_module* m, const void* const* dev_inputs, void* dev_out, void* dev_ws,
+                    int64_t ws_bytes, void* stream, int32_t n_checks, const mk_check* checks,
+                    mk_verify_report* report);
+
+const char* mk_status_str(mk_status s);
+const char* mk_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

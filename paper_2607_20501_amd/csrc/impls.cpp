@@ -1,0 +1,241 @@
+// Implementation table and subkernel dispatch.
+//
+// Every family has a tuned implementation (MK_IMPL_TUNED) and a simple one
+// (MK_IMPL_SIMPLE); a subkernel's implementation can be swapped without
+// touching the others (MKEvolve Sec. 3, "Swap").  Ids >= 100 are test-only
+// mutants reproducing the injected bugs of App. D, used to show that
+// per-stage verification catches them.
+#include "impls.hpp"
+
+#include <algorithm>
+#include <string>
+
+#include "kernels.hpp"
+
+namespace mk {
+
+enum Mutant : int32_t {
+  MUT_MASK_OFF_BY_ONE = 102,  // the diagonal is masked too
+  MUT_TILE_BOUNDARY = 103,    // the last K slice of the contraction is not loaded
+  MUT_GELU_SIGMOID = 107,     // x * sigmoid(1.702 x) instead of exact GELU
+  MUT_NO_RESIDUAL = 108,      // residual add dropped
+  MUT_RELU_FOR_GELU = 109     // ReLU instead of GELU
+};
+
+static bool chain_has(const EpiChain& c, int code) {
+  for (int i = 0; i < c.n; ++i)
+    if (c.step[i].code == code) return true;
+  return false;
+}
+
+static bool chain_has_gelu(const EpiChain& c) {
+  return chain_has(c, EPI_GELU_ERF) || chain_has(c, EPI_GELU_TANH);
+}
+
+static const EpiChain* chain_of(const Subkernel& sk) {
+  switch (sk.family) {
+    case MK_FAM_GEMM: return &sk.gemm.epi;
+    case MK_FAM_CONV: return &sk.conv.epi;
+    case MK_FAM_EW: return &sk.ew.epi;
+    case MK_FAM_ROW: return &sk.row.pre.epi;
+    default: return nullptr;
+  }
+}
+
+bool impl_exists(const Plan& p, const Subkernel& sk, int impl) {
+  (void)p;
+  if (impl == MK_IMPL_TUNED) return true;
+  if (impl == MK_IMPL_SIMPLE) {
+    if (sk.family == MK_FAM_ATTN) return sk.attn.S * 4 <= 65536;
+    return true;
+  }
+  const EpiChain* c = chain_of(sk);
+  switch (impl) {
+    case MUT_MASK_OFF_BY_ONE:
+      return (c && chain_has(*c, EPI_CAUSAL)) || (sk.family == MK_FAM_ATTN && sk.attn.causal);
+    case MUT_TILE_BOUNDARY:
+      return sk.family == MK_FAM_GEMM && sk.gemm.K > 16;
+    case MUT_GELU_SIGMOID: case MUT_RELU_FOR_GELU:
+      return c && chain_has_gelu(*c);
+    case MUT_NO_RESIDUAL:
+      return c && chain_has(*c, EPI_ADD);
+    default:
+      return false;
+  }
+}
+
+static bool use_mfma(const Plan& p, const Subkernel& sk, int impl) {
+  if (impl != MK_IMPL_TUNED || sk.family != MK_FAM_GEMM) return false;
+  GemmArgs probe{};
+  probe.M = sk.gemm.M;
+  probe.N = sk.gemm.N;
+  probe.K = sk.gemm.K;
+  probe.lda = sk.gemm.lda;
+  probe.ldb = sk.gemm.ldb;
+  probe.ldc = sk.gemm.ldc;
+  probe.layout = sk.gemm.layout;
+  probe.batch = (int32_t)sk.gemm.batch;
+  probe.heads = (int32_t)sk.gemm.heads;
+  probe.terminal = sk.gemm.terminal;
+  probe.a_off = sk.gemm.a_off; probe.a_sb = sk.gemm.a_sb; probe.a_sh = sk.gemm.a_sh;
+  probe.b_off = sk.gemm.b_off; probe.b_sb = sk.gemm.b_sb; probe.b_sh = sk.gemm.b_sh;
+  probe.c_off = sk.gemm.c_off; probe.c_sb = sk.gemm.c_sb; probe.c_sh = sk.gemm.c_sh;
+  return gemm_mfma_supported(p.dtype, probe);
+}
+
+static int64_t gemm_tiles(const Plan& p, const Subkernel& sk, int impl) {
+  const int64_t tn = use_mfma(p, sk, impl) ? kMfmaTileN : 64;
+  return (sk.gemm.N + tn - 1) / tn;
+}
+
+static int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
+
+int64_t impl_scratch(const Plan& p, const Subkernel& sk, int impl) {
+  if (sk.family != MK_FAM_GEMM) return 0;
+  const GemmSpec& g = sk.gemm;
+  int64_t b = g.ln ? align256(2 * g.M * 4) : 0;
+  if (g.terminal == TERM_ROWSUM) b += align256(g.M * gemm_tiles(p, sk, impl) * 4);
+  if (g.terminal == TERM_SOFTMAX) b += align256(g.M * gemm_tiles(p, sk, impl) * 8);
+  return b;
+}
+
+int64_t max_scratch_bytes(const Plan& p, const Subkernel& sk) {
+  return std::max(impl_scratch(p, sk, MK_IMPL_TUNED), impl_scratch(p, sk, MK_IMPL_SIMPLE));
+}
+
+int impl_launches(const Plan& p, const Subkernel& sk, int impl) {
+  (void)p;
+  (void)impl;
+  if (sk.family == MK_FAM_GEMM)
+    return 1 + (sk.gemm.ln ? 1 : 0) + (sk.gemm.terminal != TERM_NONE ? 1 : 0);
+  return 1;
+}
+
+static EpiDev resolve(const EpiChain& c, const std::vector<void*>& vals, int impl) {
+  EpiDev d{};
+  for (int i = 0; i < c.n; ++i) {
+    int code = c.step[i].code;
+    if (impl == MUT_NO_RESIDUAL && code == EPI_ADD) continue;
+    if (impl == MUT_RELU_FOR_GELU && (code == EPI_GELU_ERF || code == EPI_GELU_TANH))
+      code = EPI_RELU;
+    if (impl == MUT_GELU_SIGMOID && (code == EPI_GELU_ERF || code == EPI_GELU_TANH))
+      code = EPI_GELU_SIGMOID;
+    if (impl == MUT_MASK_OFF_BY_ONE && code == EPI_CAUSAL) code = EPI_CAUSAL_STRICT;
+    d.code[d.n] = code;
+    d.ptr[d.n] = c.step[i].value >= 0 ? vals[c.step[i].value] : nullptr;
+    d.s[d.n] = c.step[i].s;
+    ++d.n;
+  }
+  return d;
+}
+
+static EwArgs ew_args(const EwSpec& e, const std::vector<void*>& vals, void* out, int impl) {
+  EwArgs a{};
+  a.x = vals[e.x_value];
+  a.y = out;
+  a.numel = e.numel;
+  a.last = e.last;
+  a.C = e.C;
+  a.HW = e.HW;
+  a.S = e.S;
+  a.epi = resolve(e.epi, vals, impl);
+  return a;
+}
+
+static mk_status hip_check(hipError_t e, const char* what) {
+  if (e == hipSuccess) return MK_OK;
+  return fail(MK_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<void*>& vals,
+                        void* out, void* scratch, hipStream_t st) {
+  const int impl = sk.impl;
+  const int dt = p.dtype;
+  switch (sk.family) {
+    case MK_FAM_EW:
+      return hip_check(launch_ew(dt, ew_args(sk.ew, vals, out, impl), st), "element-wise");
+    case MK_FAM_ROW: {
+      const RowSpec& r = sk.row;
+      RowArgs a{};
+      a.x = vals[r.x_value];
+      a.y = out;
+      a.rows = r.rows;
+      a.len = r.len;
+      a.op = r.op;
+      a.gamma = r.g_value >= 0 ? vals[r.g_value] : nullptr;
+      a.beta = r.b_value >= 0 ? vals[r.b_value] : nullptr;
+      a.eps = r.eps;
+      a.pre = ew_args(r.pre, vals, nullptr, impl);
+      return hip_check(launch_row(dt, a, st, impl), "row");
+    }
+    case MK_FAM_GEMM: {
+      const GemmSpec& g = sk.gemm;
+      GemmArgs a{};
+      a.A = vals[g.a_value];
+      a.B = vals[g.b_value];
+      a.C = out;
+      a.M = g.M; a.N = g.N; a.K = g.K;
+      a.lda = g.lda; a.ldb = g.ldb; a.ldc = g.ldc;
+      a.a_off = g.a_off; a.a_sb = g.a_sb; a.a_sh = g.a_sh;
+      a.b_off = g.b_off; a.b_sb = g.b_sb; a.b_sh = g.b_sh;
+      a.c_off = g.c_off; a.c_sb = g.c_sb; a.c_sh = g.c_sh;
+      a.batch = (int32_t)g.batch;
+      a.heads = (int32_t)g.heads;
+      a.layout = g.layout;
+      a.terminal = g.terminal;
+      a.alpha = g.alpha;
+      a.epi = resolve(g.epi, vals, impl);
+      if (impl == MUT_TILE_BOUNDARY) a.K = g.K - ((g.K % 16) ? (g.K % 16) : 16);
+      char* sc = (char*)scratch;
+      if (g.ln) {
+        float* stats = (float*)sc;
+        sc += align256(2 * g.M * 4);
+        mk_status s = hip_check(launch_ln_stats(dt, vals[g.a_value], g.M, g.K, g.eps, stats, st),
+                                "layernorm stats");
+        if (s != MK_OK) return s;
+        a.ln_stats = stats;
+        a.ln_g = vals[g.ln_g];
+        a.ln_b = vals[g.ln_b];
+      }
+      a.partial = (float*)sc;
+      a.n_tiles = gemm_tiles(p, sk, impl);
+      const bool mfma = use_mfma(p, sk, impl);
+      mk_status s = hip_check(mfma ? launch_gemm_mfma(dt, a, st) : launch_gemm_simple(dt, a, st),
+                              "gemm");
+      if (s != MK_OK) return s;
+      if (g.terminal == TERM_ROWSUM)
+        return hip_check(launch_rowsum_finish(dt, a.partial, g.M, a.n_tiles, out, st),
+                         "row-sum finish");
+      if (g.terminal == TERM_SOFTMAX)
+        return hip_check(launch_softmax_finish(dt, a.partial, g.M, a.n_tiles, g.N, out, st),
+                         "softmax finish");
+      return MK_OK;
+    }
+    case MK_FAM_CONV: {
+      const ConvSpec& c = sk.conv;
+      ConvArgs a{};
+      a.x = vals[c.x_value];
+      a.w = vals[c.w_value];
+      a.y = out;
+      a.N = c.N; a.C = c.C; a.H = c.H; a.W = c.W; a.K = c.K; a.R = c.R; a.S = c.S;
+      a.P = c.P; a.Q = c.Q; a.stride = c.stride; a.pad = c.pad;
+      a.epi = resolve(c.epi, vals, impl);
+      a.gap = c.gap ? 1 : 0;
+      return hip_check(launch_conv_simple(dt, a, st), "conv");
+    }
+    case MK_FAM_ATTN: {
+      const AttnSpec& t = sk.attn;
+      AttnArgs a{};
+      a.qkv = vals[t.qkv_value];
+      a.o = out;
+      a.B = t.B; a.H = t.H; a.dh = t.dh; a.S = t.S;
+      a.scale = t.scale;
+      a.causal = t.causal ? (impl == MUT_MASK_OFF_BY_ONE ? 2 : 1) : 0;
+      return hip_check(launch_attn_simple(dt, a, st), "attention");
+    }
+    default:
+      return fail(MK_E_INTERNAL, "unknown family");
+  }
+}
+
+}  // namespace mk

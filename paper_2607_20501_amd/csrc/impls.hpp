@@ -1,0 +1,25 @@
+// Implementation table: for each subkernel family, the implementations that
+// can run a matched group, their launch counts and scratch needs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <vector>
+
+#include "plan.hpp"
+
+namespace mk {
+
+bool impl_exists(const Plan& p, const Subkernel& sk, int impl);
+int impl_launches(const Plan& p, const Subkernel& sk, int impl);
+int64_t impl_scratch(const Plan& p, const Subkernel& sk, int impl);
+// Largest scratch over the implementations of sk (so a swap never needs a
+// bigger workspace).
+int64_t max_scratch_bytes(const Plan& p, const Subkernel& sk);
+
+// Enqueue subkernel sk.  vals[v] is the device pointer of value v (null for
+// values no buffer holds), out the subkernel's output buffer.
+mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<void*>& vals,
+                        void* out, void* scratch, hipStream_t st);
+
+}  // namespace mk

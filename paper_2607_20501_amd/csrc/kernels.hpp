@@ -1,0 +1,93 @@
+// Launch interfaces of the HIP kernels.  Plain pointers and sizes; every
+// launcher enqueues on `stream` and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/mk.h"
+
+namespace mk {
+
+// Element-wise chain as the kernels see it (codes from plan.hpp's EpiCode).
+struct EpiDev {
+  int32_t n;
+  int32_t code[8];
+  const void* ptr[8];
+  float s[8];
+};
+
+struct EwArgs {
+  const void* x;
+  void* y;
+  int64_t numel, last, C, HW, S;
+  EpiDev epi;
+};
+
+// One row op per row of a [rows, len] view (GAP: rows = N*C, len = H*W).
+struct RowArgs {
+  const void* x;
+  void* y;
+  int64_t rows, len;
+  int32_t op;              // MK_OP_ROWSUM / SOFTMAX / LAYERNORM / GAP
+  const void* gamma;
+  const void* beta;
+  float eps;
+  EwArgs pre;              // element-wise prologue (pre.epi.n == 0: none)
+};
+
+struct GemmArgs {
+  const void* A;
+  const void* B;
+  void* C;
+  int64_t M, N, K, lda, ldb, ldc;
+  int64_t a_off, a_sb, a_sh, b_off, b_sb, b_sh, c_off, c_sb, c_sh;
+  int32_t batch, heads, layout, terminal;
+  float alpha;
+  const float* ln_stats;   // [M][2] (mean, rstd) of A's rows, or null
+  const void* ln_g;
+  const void* ln_b;
+  EpiDev epi;
+  float* partial;          // row partials of the terminal reduction
+  int64_t n_tiles;         // column tiles per row in `partial`
+};
+
+struct ConvArgs {
+  const void* x;
+  const void* w;
+  void* y;
+  int64_t N, C, H, W, K, R, S, P, Q, stride, pad;
+  EpiDev epi;              // channel-indexed chain
+  int32_t gap;
+  float* partial;          // GAP partial sums [N][K][n_pos_tiles]
+  int64_t n_pos_tiles;
+  void* scratch;           // tuned conv: repacked operands
+};
+
+struct AttnArgs {
+  const void* qkv;
+  void* o;
+  int64_t B, H, dh, S;
+  float scale;
+  int32_t causal;
+};
+
+// dtype: 0 float32, 1 bfloat16 (mk_dtype).
+hipError_t launch_ew(int dtype, const EwArgs& a, hipStream_t st);
+hipError_t launch_row(int dtype, const RowArgs& a, hipStream_t st, int impl);
+hipError_t launch_ln_stats(int dtype, const void* x, int64_t rows, int64_t len, float eps,
+                           float* stats, hipStream_t st);
+hipError_t launch_gemm_simple(int dtype, const GemmArgs& a, hipStream_t st);
+hipError_t launch_rowsum_finish(int dtype, const float* partial, int64_t rows, int64_t n_tiles,
+                                void* out, hipStream_t st);
+hipError_t launch_softmax_finish(int dtype, const float* partial, int64_t rows, int64_t n_tiles,
+                                 int64_t N, void* out, hipStream_t st);
+hipError_t launch_conv_simple(int dtype, const ConvArgs& a, hipStream_t st);
+hipError_t launch_attn_simple(int dtype, const AttnArgs& a, hipStream_t st);
+
+// Tuned kernels.
+constexpr int64_t kMfmaTileN = 256;   // column tile of the bf16 MFMA GEMM
+bool gemm_mfma_supported(int dtype, const GemmArgs& a);
+hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st);
+
+}  // namespace mk
