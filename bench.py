@@ -1,0 +1,206 @@
+#!/usr/bin/env python3
+"""Composed-module benchmark on one MI355X.
+
+A step is one run of the whole composed module (every subkernel of the
+chosen decomposition) over one batch of synthetic, seeded input that is
+already resident in HBM.  Default workload: the bf16 module
+x[8192,4096] @ W[4096,4096] + b, tanh-GELU, scale 0.5, row softmax, fused.
+
+Prints ONE JSON line with the throughput of the fused composition (TFLOP/s of
+the module's algorithmic flops), the split composition beside it, the
+roofline of the dominant kernel (from HIP events around each launch, recorded
+live over the timed steps) and the oracle's CPU throughput on a bounded row
+sample (which also checks those rows of the GPU output).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6    # 256 CU x 2.4 GHz x 4096 flop/clk/CU, dense
+PEAK_F32_TFLOPS = 157.3      # fp32 matrix
+PEAK_HBM_GBS = 8000.0
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def build_module(cfg, dtype):
+    from paper_2607_20501_amd import workloads
+    if cfg == 3:
+        return workloads.conv_relu_gap(dtype=dtype or "bf16")
+    m = workloads.full_size(cfg)
+    if dtype:
+        m["dtype"] = dtype
+    return m
+
+
+def launch_names(mod):
+    """Name of every kernel launch of one run, in order."""
+    names = []
+    for s in mod.subkernels():
+        ops = [o["kind"] for o in mod.desc["ops"][s["op_begin"]:s["op_end"]]]
+        if s["family"] == "GEMM":
+            seq = ["layernorm prologue (row_kernel)"] if ops[0] == "LAYERNORM" else []
+            seq.append("gemm_bf16_mfma_kernel (fused epilogue: " + ",".join(ops) + ")")
+            if ops[-1] in ("SOFTMAX", "ROWSUM"):
+                seq.append(ops[-1].lower() + "_finish_kernel")
+            names += seq[:s["n_launches"]] + ["?"] * (s["n_launches"] - len(seq))
+        else:
+            names += [s["family"].lower() + " subkernel (" + ",".join(ops) + ")"] * s["n_launches"]
+    return names
+
+
+def time_module(mod, ins, out, ws, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        mod.run(ins, out, ws)
+    torch.cuda.synchronize()
+    per_run = mod.launches_per_run()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    mod.profile_begin(per_run * steps)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        mod.run(ins, out, ws)
+    end.record()
+    torch.cuda.synchronize()
+    launch_ms = mod.profile_end(per_run * steps)
+    ms = start.elapsed_time(end) / steps
+    per_launch = [sum(launch_ms[k::per_run]) / steps for k in range(per_run)]
+    return ms, per_launch
+
+
+def cpu_baseline(module, host, rows, out_dev):
+    """The oracle on the first `rows` rows of a row-independent module; also
+    compares those rows of the GPU output."""
+    import numpy as np
+    import oracle
+    from paper_2607_20501_amd import mk
+    sub = json.loads(json.dumps(module))
+    M = module["inputs"][0][0]
+    rows = min(rows, M)
+    sub["inputs"][0][0] = rows
+    K = module["inputs"][0][1]
+    sub_host = [host[0][:rows * K]] + list(host[1:])
+    groups = mk.mk_decomposition_preset(module, "fused")
+    threads = os.cpu_count() or 1
+    t = time.perf_counter()
+    ref = oracle.run(sub, groups, sub_host, keep={len(module["ops"]) - 1}, nthreads=threads)[-1]
+    dt = time.perf_counter() - t
+    flops = oracle.plan(sub, groups)["flops"]
+    got = mk.to_float64(out_dev[:rows])
+    err = np.abs(got - ref)
+    tol = 2e-2 * np.abs(ref) + 2e-2 / ref.shape[-1]
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} of {M} rows of the same fused module (fp64 oracle, "
+                      f"{flops / 1e9:.1f} GFLOP in {dt:.1f} s)",
+            "seconds": dt,
+            "parity_rows_checked": rows, "parity_max_abs_err": float(err.max()),
+            "parity_pass": bool((err <= tol).all())}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--dtype", default=None, choices=[None, "f32", "bf16"])
+    ap.add_argument("--decomp", default="fused", choices=["fused", "split"])
+    ap.add_argument("--no-split", action="store_true", help="skip timing the split form")
+    ap.add_argument("--cpu-rows", type=int, default=None,
+                    help="rows of the oracle sample (default: about 30 GFLOP of work)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: the composed-module hot path is "
+              "single-GPU (no collectives); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_20501_amd import inputs, mk
+
+    torch.cuda.set_device(0)
+    module = build_module(args.config, args.dtype)
+    t0 = time.perf_counter()
+    host = inputs.make_inputs(module, args.seed)
+    log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
+    fused = mk.Module(module, args.decomp)
+    split = None if args.no_split else mk.Module(module, "split")
+    ws_bytes = max(fused.workspace_size(), split.workspace_size() if split else 0)
+    ins, _, ws = mk.device_buffers(module, host, ws_bytes)
+    out = mk.out_tensor(module, fused.info["out_shape"])
+    flops = fused.info["flops"]
+
+    ms, per_launch = time_module(fused, ins, out, ws, args.steps, args.warmup)
+    log(f"{args.decomp}: {ms * 1e3:.1f} us/step, launches (us): "
+        f"{[round(x * 1e3, 1) for x in per_launch]}")
+    result = {}
+    if split is not None:
+        out_s = mk.out_tensor(module, split.info["out_shape"])
+        ms_s, per_s = time_module(split, ins, out_s, ws, args.steps, args.warmup)
+        log(f"split: {ms_s * 1e3:.1f} us/step, launches (us): {[round(x * 1e3, 1) for x in per_s]}")
+        result["split"] = {"ms_per_step": ms_s, "value": flops / (ms_s * 1e-3) / 1e12,
+                           "launch_us": [round(x * 1e3, 2) for x in per_s]}
+        result["fused_vs_split_speedup"] = ms_s / ms
+        # the split run overwrote nothing the fused output depends on; rerun fused
+        fused.run(ins, out, ws)
+        torch.cuda.synchronize()
+
+    # dominant kernel of the timed composition
+    names = launch_names(fused)
+    k = max(range(len(per_launch)), key=lambda i: per_launch[i])
+    sk = fused.subkernels()
+    launch_to_sub = [i for i, s in enumerate(sk) for _ in range(s["n_launches"])]
+    sub = sk[launch_to_sub[k]]
+    bf = module["dtype"] == "bf16"
+    if sub["flops"] > 0:
+        achieved = sub["flops"] / (per_launch[k] * 1e-3) / 1e12
+        peak = PEAK_BF16_TFLOPS if bf else PEAK_F32_TFLOPS
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                "frac": achieved / peak, "traffic": None}
+    else:
+        achieved = sub["alg_bytes"] / (per_launch[k] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS, "traffic": None}
+    roof["kernel"] = names[k]
+    roof["kernel_us"] = per_launch[k] * 1e3
+    roof["per_launch_flops"] = sub["flops"]
+    roof["per_launch_alg_bytes"] = sub["alg_bytes"]
+
+    line = {
+        "metric": "composed-module TFLOP/s (fused), % of MI355X roofline, fused vs split speedup",
+        "value": flops / (ms * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf else "f32",
+        "data": "synthetic (seeded SplitMix64 / Box-Muller inputs, resident in HBM)",
+        "config": {"workload": module["name"], "decomposition": args.decomp,
+                   "module_flops": flops, "module_alg_bytes": fused.info["alg_bytes"],
+                   "launches_per_step": len(per_launch), "parallelism": "single GPU"},
+        "roofline": roof,
+        "launch_us": [round(x * 1e3, 2) for x in per_launch],
+    }
+    line.update(result)
+    if not args.no_cpu_baseline and args.config in (1, 2, 4):
+        M = module["inputs"][0][0]
+        rows = args.cpu_rows or max(1, min(M, int(30e9 / (flops / M))))
+        line["cpu_baseline"] = cpu_baseline(module, host, rows, out)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -167,6 +167,18 @@ mk_status mk_workspace_size(const mk_module* m, int64_t* bytes);
 mk_status mk_run(mk_module* m, const void* const* dev_inputs, void* dev_out, void* dev_ws,
                  int64_t ws_bytes, void* stream, float* per_subkernel_ms);
 
+/* Launch-level profiling (timing of each kernel launch, for roofline
+ * figures).  While a profile is open, every mk_run of the module also brackets
+ * each of its kernel launches with HIP events, without synchronising, until
+ * max_launches launches are recorded (later launches are not recorded).
+ * mk_profile_end synchronises on the last recorded launch, writes the elapsed
+ * milliseconds of the recorded launches in launch order to launch_ms (at most
+ * capacity entries), sets *n_recorded and closes the profile.  A run
+ * contributes sum(mk_subkernel_info.n_launches) consecutive entries.
+ * MK_E_INVALID_ARG if a profile is already open / not open. */
+mk_status mk_profile_begin(mk_module* m, int32_t max_launches);
+mk_status mk_profile_end(mk_module* m, float* launch_ms, int32_t capacity, int32_t* n_recorded);
+
 /* One reference check: stage s is subkernel s's materialised output (the last
  * subkernel's is the module output).  Element index[k] (flat, row-major; NULL
  * means index k) of that tensor must satisfy

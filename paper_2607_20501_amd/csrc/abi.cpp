@@ -24,10 +24,14 @@ const char* last_error();
 
 struct mk_module {
   mk::Plan plan;
-  std::vector<hipEvent_t> events;
+  std::vector<hipEvent_t> events;   // per-subkernel timing
   int event_device = -1;
+  std::vector<hipEvent_t> prof;     // launch-level profile (2 per launch)
+  mk::LaunchTimer timer;
+  bool profiling = false;
   ~mk_module() {
     for (hipEvent_t e : events) (void)hipEventDestroy(e);
+    for (hipEvent_t e : prof) (void)hipEventDestroy(e);
   }
 };
 
@@ -193,7 +197,12 @@ mk_status mk_run(mk_module* m, const void* const* dev_inputs, void* dev_out, voi
         hipError_t e = hipEventRecord(m->events[2 * i], st);
         if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
       }
-      s = mk::run_subkernel(p, sk, vals, vals[sk.out_value], scratch, st);
+      mk::LaunchTimer* tm = nullptr;
+      if (m->profiling) {
+        m->timer.stream = st;
+        tm = &m->timer;
+      }
+      s = mk::run_subkernel(p, sk, vals, vals[sk.out_value], scratch, st, tm);
       if (s != MK_OK) return s;
       if (per_subkernel_ms) {
         hipError_t e = hipEventRecord(m->events[2 * i + 1], st);
@@ -212,6 +221,41 @@ mk_status mk_run(mk_module* m, const void* const* dev_inputs, void* dev_out, voi
   } catch (...) {
     return fail(MK_E_INTERNAL, "exception in mk_run");
   }
+}
+
+mk_status mk_profile_begin(mk_module* m, int32_t max_launches) {
+  if (!m || max_launches < 1) return fail(MK_E_INVALID_ARG, "null module or max_launches < 1");
+  if (m->profiling) return fail(MK_E_INVALID_ARG, "a profile is already open");
+  for (hipEvent_t e : m->prof) (void)hipEventDestroy(e);
+  m->prof.assign(2 * (size_t)max_launches, nullptr);
+  for (auto& e : m->prof) {
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) {
+      e = nullptr;
+      return hip_fail(r, "hipEventCreate");
+    }
+  }
+  m->timer.events = &m->prof;
+  m->timer.next = 0;
+  m->profiling = true;
+  return MK_OK;
+}
+
+mk_status mk_profile_end(mk_module* m, float* launch_ms, int32_t capacity, int32_t* n_recorded) {
+  if (!m || !n_recorded || (capacity > 0 && !launch_ms))
+    return fail(MK_E_INVALID_ARG, "null argument");
+  if (!m->profiling) return fail(MK_E_INVALID_ARG, "no profile is open");
+  m->profiling = false;
+  const int32_t n = (int32_t)(m->timer.next / 2);
+  *n_recorded = n;
+  if (n == 0) return MK_OK;
+  hipError_t e = hipEventSynchronize(m->prof[2 * n - 1]);
+  if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  for (int32_t i = 0; i < n && i < capacity; ++i) {
+    e = hipEventElapsedTime(&launch_ms[i], m->prof[2 * i], m->prof[2 * i + 1]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+  }
+  return MK_OK;
 }
 
 static double decode(int32_t dtype, const uint8_t* base, int64_t i) {

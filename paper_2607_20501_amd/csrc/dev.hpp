@@ -37,20 +37,43 @@ template <typename T> __device__ __forceinline__ float rnd(float v);
 template <> __device__ __forceinline__ float rnd<float>(float v) { return v; }
 template <> __device__ __forceinline__ float rnd<bf16>(float v) { return bf2f(f2bf(v)); }
 
-__device__ __forceinline__ float gelu_erf(float x) {
-  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, 7.1.26:
+// erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
+// t = 1 / (1 + p x) for x >= 0 (|error| <= 1.5e-7), odd extension for x < 0.
+__device__ __forceinline__ float erf_as(float x) {
+  const float ax = fabsf(x);
+  const float t = __frcp_rn(1.0f + 0.3275911f * ax);
+  float poly = 1.061405429f;
+  poly = fmaf(poly, t, -1.453152027f);
+  poly = fmaf(poly, t, 1.421413741f);
+  poly = fmaf(poly, t, -0.284496736f);
+  poly = fmaf(poly, t, 0.254829592f);
+  poly *= t;
+  const float y = 1.0f - poly * __expf(-ax * ax);
+  return copysignf(y, x);
 }
+
+__device__ __forceinline__ float gelu_erf(float x) {
+  return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f));
+}
+// 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)) exactly, so the tanh form of GELU is
+// x * sigmoid(2u) with u = sqrt(2/pi) (x + 0.044715 x^3).
 __device__ __forceinline__ float gelu_tanh(float x) {
-  const float c = 0.79788456080286536f;  // sqrt(2 / pi)
-  return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
+  const float c2 = 1.5957691216057308f;  // 2 sqrt(2 / pi)
+  const float u2 = c2 * (x + 0.044715f * x * x * x);
+  return x / (1.0f + __expf(-u2));
 }
 
 // Apply the chain to v.  col: column (BIAS_COL); ch: channel (BIAS_CH);
 // flat: element offset shared with residual operands; (row, col) for CAUSAL.
+// The loop over the (at most kMaxEpi) steps is unrolled so that the step codes
+// are read once per kernel, not once per element.
 template <typename T>
 __device__ __forceinline__ float epi_apply(const EpiDev& e, float v, int64_t row, int64_t col,
                                            int64_t ch, int64_t flat) {
-  for (int i = 0; i < e.n; ++i) {
+#pragma unroll
+  for (int i = 0; i < kMaxEpi; ++i) {
+    if (i >= e.n) break;
     switch (e.code[i]) {
       case EPI_BIAS_COL: v += ld<T>((const T*)e.ptr[i], col); break;
       case EPI_BIAS_CH: v += ld<T>((const T*)e.ptr[i], ch); break;
@@ -66,6 +89,87 @@ __device__ __forceinline__ float epi_apply(const EpiDev& e, float v, int64_t row
     }
   }
   return v;
+}
+
+// Load 8 consecutive values p[0..7] as floats; `vec` allows one 16-byte (bf16)
+// or two 16-byte (fp32) accesses, otherwise only the first `valid` are read.
+template <typename T>
+__device__ __forceinline__ void ld8(const T* p, bool vec, int valid, float (&out)[8]) {
+  if (vec) {
+    if constexpr (sizeof(T) == 2) {
+      const uint4 r = *(const uint4*)p;
+      const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        out[2 * k] = __uint_as_float(w[k] << 16);
+        out[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
+      }
+    } else {
+      const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+      out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+      out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) out[k] = k < valid ? ld<T>(p, k) : 0.f;
+  }
+}
+
+// The chain applied to 8 consecutive columns col0.. of one row (flat0 is the
+// offset of column col0 in residual operands).  One uniform switch per step;
+// `vec` says that 16-byte operand accesses are aligned and in range.
+template <typename T>
+__device__ __forceinline__ void epi_apply8(const EpiDev& e, float (&v)[8], int64_t row,
+                                           int64_t col0, int valid, int64_t flat0, bool vec) {
+#pragma unroll
+  for (int i = 0; i < kMaxEpi; ++i) {
+    if (i >= e.n) break;
+    float t[8];
+    switch (e.code[i]) {
+      case EPI_BIAS_COL:
+        ld8<T>((const T*)e.ptr[i] + col0, vec, valid, t);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] += t[k];
+        break;
+      case EPI_ADD:
+        ld8<T>((const T*)e.ptr[i] + flat0, vec, valid, t);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] += t[k];
+        break;
+      case EPI_RELU:
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = fmaxf(v[k], 0.0f);
+        break;
+      case EPI_GELU_ERF:
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = gelu_erf(v[k]);
+        break;
+      case EPI_GELU_TANH:
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = gelu_tanh(v[k]);
+        break;
+      case EPI_SCALE:
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] *= e.s[i];
+        break;
+      case EPI_CAUSAL:
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (col0 + k > row) v[k] = -INFINITY;
+        break;
+      case EPI_GELU_SIGMOID:
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = v[k] / (1.0f + __expf(-1.702f * v[k]));
+        break;
+      case EPI_CAUSAL_STRICT:
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (col0 + k >= row) v[k] = -INFINITY;
+        break;
+      default:
+        break;
+    }
+  }
 }
 
 __device__ __forceinline__ float warp_sum(float v) {

@@ -83,20 +83,34 @@ static bool use_mfma(const Plan& p, const Subkernel& sk, int impl) {
   return gemm_mfma_supported(p.dtype, probe);
 }
 
-static int64_t gemm_tiles(const Plan& p, const Subkernel& sk, int impl) {
-  const int64_t tn = use_mfma(p, sk, impl) ? kMfmaTileN : 64;
-  return (sk.gemm.N + tn - 1) / tn;
-}
-
 static int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
+
+// Scratch layout of a GEMM subkernel: [LayerNorm region][row partials].
+// The MFMA path applies a LayerNorm prologue as a pre-pass that writes the
+// normalised rows (storage dtype) to scratch; the simple path keeps per-row
+// (mean, rstd) and normalises while loading A.
+struct GemmScratch {
+  bool mfma;
+  int64_t n_tiles, ln_bytes, bt_bytes, partial_bytes;
+};
+
+static GemmScratch gemm_scratch(const Plan& p, const Subkernel& sk, int impl) {
+  const GemmSpec& g = sk.gemm;
+  GemmScratch s{};
+  s.mfma = use_mfma(p, sk, impl);
+  const int64_t tn = s.mfma ? kMfmaTileN : 64;
+  s.n_tiles = (g.N + tn - 1) / tn;
+  if (g.ln) s.ln_bytes = align256(s.mfma ? g.M * g.K * elem_size(p.dtype) : 2 * g.M * 4);
+  if (s.mfma && g.layout == 1) s.bt_bytes = align256(g.batch * g.heads * g.N * g.K * 2);
+  if (g.terminal == TERM_ROWSUM) s.partial_bytes = align256(g.M * s.n_tiles * 4);
+  if (g.terminal == TERM_SOFTMAX) s.partial_bytes = align256(g.M * s.n_tiles * 8);
+  return s;
+}
 
 int64_t impl_scratch(const Plan& p, const Subkernel& sk, int impl) {
   if (sk.family != MK_FAM_GEMM) return 0;
-  const GemmSpec& g = sk.gemm;
-  int64_t b = g.ln ? align256(2 * g.M * 4) : 0;
-  if (g.terminal == TERM_ROWSUM) b += align256(g.M * gemm_tiles(p, sk, impl) * 4);
-  if (g.terminal == TERM_SOFTMAX) b += align256(g.M * gemm_tiles(p, sk, impl) * 8);
-  return b;
+  const GemmScratch s = gemm_scratch(p, sk, impl);
+  return s.ln_bytes + s.bt_bytes + s.partial_bytes;
 }
 
 int64_t max_scratch_bytes(const Plan& p, const Subkernel& sk) {
@@ -104,10 +118,11 @@ int64_t max_scratch_bytes(const Plan& p, const Subkernel& sk) {
 }
 
 int impl_launches(const Plan& p, const Subkernel& sk, int impl) {
-  (void)p;
-  (void)impl;
-  if (sk.family == MK_FAM_GEMM)
-    return 1 + (sk.gemm.ln ? 1 : 0) + (sk.gemm.terminal != TERM_NONE ? 1 : 0);
+  if (sk.family == MK_FAM_GEMM) {
+    const bool transpose = use_mfma(p, sk, impl) && sk.gemm.layout == 1;
+    return 1 + (sk.gemm.ln ? 1 : 0) + (transpose ? 1 : 0) +
+           (sk.gemm.terminal != TERM_NONE ? 1 : 0);
+  }
   return 1;
 }
 
@@ -148,12 +163,20 @@ static mk_status hip_check(hipError_t e, const char* what) {
 }
 
 mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<void*>& vals,
-                        void* out, void* scratch, hipStream_t st) {
+                        void* out, void* scratch, hipStream_t st, LaunchTimer* tm) {
+  // Each launch is bracketed by tm->mark() when launch timing is active.
+  auto timed = [tm](auto&& launch) {
+    if (tm) tm->mark();
+    hipError_t e = launch();
+    if (tm) tm->mark();
+    return e;
+  };
   const int impl = sk.impl;
   const int dt = p.dtype;
   switch (sk.family) {
     case MK_FAM_EW:
-      return hip_check(launch_ew(dt, ew_args(sk.ew, vals, out, impl), st), "element-wise");
+      return hip_check(timed([&] { return launch_ew(dt, ew_args(sk.ew, vals, out, impl), st); }),
+                       "element-wise");
     case MK_FAM_ROW: {
       const RowSpec& r = sk.row;
       RowArgs a{};
@@ -166,7 +189,7 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       a.beta = r.b_value >= 0 ? vals[r.b_value] : nullptr;
       a.eps = r.eps;
       a.pre = ew_args(r.pre, vals, nullptr, impl);
-      return hip_check(launch_row(dt, a, st, impl), "row");
+      return hip_check(timed([&] { return launch_row(dt, a, st, impl); }), "row");
     }
     case MK_FAM_GEMM: {
       const GemmSpec& g = sk.gemm;
@@ -186,28 +209,66 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       a.alpha = g.alpha;
       a.epi = resolve(g.epi, vals, impl);
       if (impl == MUT_TILE_BOUNDARY) a.K = g.K - ((g.K % 16) ? (g.K % 16) : 16);
+      const GemmScratch gs = gemm_scratch(p, sk, impl);
+      const bool aligned = ((uintptr_t)a.B % 16 == 0) && ((uintptr_t)vals[g.a_value] % 16 == 0);
+      if (gs.mfma && !aligned) return fail(MK_E_INVALID_ARG, "GEMM operands must be 16-byte aligned");
       char* sc = (char*)scratch;
       if (g.ln) {
-        float* stats = (float*)sc;
-        sc += align256(2 * g.M * 4);
-        mk_status s = hip_check(launch_ln_stats(dt, vals[g.a_value], g.M, g.K, g.eps, stats, st),
-                                "layernorm stats");
+        if (gs.mfma) {
+          RowArgs r{};
+          r.x = vals[g.a_value];
+          r.y = sc;
+          r.rows = g.M;
+          r.len = g.K;
+          r.op = MK_OP_LAYERNORM;
+          r.gamma = vals[g.ln_g];
+          r.beta = vals[g.ln_b];
+          r.eps = g.eps;
+          r.pre.last = r.pre.S = r.pre.C = r.pre.HW = 1;
+          mk_status s = hip_check(timed([&] { return launch_row(dt, r, st, MK_IMPL_TUNED); }),
+                                  "layernorm prologue");
+          if (s != MK_OK) return s;
+          a.A = sc;
+        } else {
+          float* stats = (float*)sc;
+          mk_status s = hip_check(timed([&] {
+                                    return launch_ln_stats(dt, vals[g.a_value], g.M, g.K, g.eps,
+                                                           stats, st);
+                                  }),
+                                  "layernorm stats");
+          if (s != MK_OK) return s;
+          a.ln_stats = stats;
+          a.ln_g = vals[g.ln_g];
+          a.ln_b = vals[g.ln_b];
+        }
+        sc += gs.ln_bytes;
+      }
+      if (gs.bt_bytes) {
+        void* bt = sc;
+        mk_status s = hip_check(timed([&] { return launch_transpose_b(a, bt, st); }),
+                                "transpose B");
         if (s != MK_OK) return s;
-        a.ln_stats = stats;
-        a.ln_g = vals[g.ln_g];
-        a.ln_b = vals[g.ln_b];
+        a = gemm_with_bt(a, bt);
+        sc += gs.bt_bytes;
       }
       a.partial = (float*)sc;
-      a.n_tiles = gemm_tiles(p, sk, impl);
-      const bool mfma = use_mfma(p, sk, impl);
-      mk_status s = hip_check(mfma ? launch_gemm_mfma(dt, a, st) : launch_gemm_simple(dt, a, st),
+      a.n_tiles = gs.n_tiles;
+      mk_status s = hip_check(timed([&] {
+                                return gs.mfma ? launch_gemm_mfma(dt, a, st)
+                                               : launch_gemm_simple(dt, a, st);
+                              }),
                               "gemm");
       if (s != MK_OK) return s;
       if (g.terminal == TERM_ROWSUM)
-        return hip_check(launch_rowsum_finish(dt, a.partial, g.M, a.n_tiles, out, st),
+        return hip_check(timed([&] {
+                           return launch_rowsum_finish(dt, a.partial, g.M, a.n_tiles, out, st);
+                         }),
                          "row-sum finish");
       if (g.terminal == TERM_SOFTMAX)
-        return hip_check(launch_softmax_finish(dt, a.partial, g.M, a.n_tiles, g.N, out, st),
+        return hip_check(timed([&] {
+                           return launch_softmax_finish(dt, a.partial, g.M, a.n_tiles, g.N, out,
+                                                        st);
+                         }),
                          "softmax finish");
       return MK_OK;
     }
@@ -221,7 +282,7 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       a.P = c.P; a.Q = c.Q; a.stride = c.stride; a.pad = c.pad;
       a.epi = resolve(c.epi, vals, impl);
       a.gap = c.gap ? 1 : 0;
-      return hip_check(launch_conv_simple(dt, a, st), "conv");
+      return hip_check(timed([&] { return launch_conv_simple(dt, a, st); }), "conv");
     }
     case MK_FAM_ATTN: {
       const AttnSpec& t = sk.attn;
@@ -231,7 +292,7 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       a.B = t.B; a.H = t.H; a.dh = t.dh; a.S = t.S;
       a.scale = t.scale;
       a.causal = t.causal ? (impl == MUT_MASK_OFF_BY_ONE ? 2 : 1) : 0;
-      return hip_check(launch_attn_simple(dt, a, st), "attention");
+      return hip_check(timed([&] { return launch_attn_simple(dt, a, st); }), "attention");
     }
     default:
       return fail(MK_E_INTERNAL, "unknown family");

@@ -17,9 +17,20 @@ int64_t impl_scratch(const Plan& p, const Subkernel& sk, int impl);
 // bigger workspace).
 int64_t max_scratch_bytes(const Plan& p, const Subkernel& sk);
 
+// Optional launch-level timing: brackets each kernel launch with a pair of
+// HIP events taken from a pre-created pool (no synchronisation).
+struct LaunchTimer {
+  std::vector<hipEvent_t>* events = nullptr;  // 2 per launch
+  size_t next = 0;                            // next free event
+  hipStream_t stream = nullptr;
+  void mark() {
+    if (events && next < events->size()) (void)hipEventRecord((*events)[next++], stream);
+  }
+};
+
 // Enqueue subkernel sk.  vals[v] is the device pointer of value v (null for
 // values no buffer holds), out the subkernel's output buffer.
 mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<void*>& vals,
-                        void* out, void* scratch, hipStream_t st);
+                        void* out, void* scratch, hipStream_t st, LaunchTimer* timer);
 
 }  // namespace mk

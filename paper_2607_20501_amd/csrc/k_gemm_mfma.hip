@@ -1,5 +1,462 @@
+// bf16 GEMM with fused epilogue on gfx950 matrix cores.
+//
+//   C[z][m, n] = chain(alpha * sum_k A[z][m, k] B[z](k, n))     (fp32 accumulate)
+//
+// The contraction is the dense GEMM of a Linear layer / conv / attention
+// product (MKEvolve App. H.2 linear kernels; the fusion guidance of App. I.1:
+// GEMM followed by bias, activations, scaling and the residual add in one
+// kernel, never materialising the intermediate).  A terminal row reduction
+// that needs a full row (softmax, row-sum) is split at the column tile: the
+// epilogue emits per-(row, tile) partials and a finisher combines them
+// (App. I.1: "may need split at softmax due to reduction").
+//
+// Design for CDNA4:
+//  * 256 x 256 output tile per workgroup, K in 32-deep slices; 4 waves in a
+//    2 x 2 arrangement, each owning 128 x 128 = 4 x 4 tiles of
+//    v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane).
+//  * Operands move HBM -> LDS with buffer_load ... lds (no register staging):
+//    a 4-stage ring of 32 KB slices keeps three slices in flight while the
+//    MFMAs consume the fourth; one barrier per slice.  Out-of-range lanes read
+//    zeros through the buffer descriptor's range check (ragged M / N / K).
+//  * LDS rows are 64 bytes (four 16-byte chunks); chunk c of row r sits at
+//    chunk c ^ (((r >> 1) ^ (r >> 3)) & 3), so the lanes served together by a
+//    128-bit fragment read hit distinct banks.  Each lane's global address is
+//    chosen so that the lane-ordered LDS write lands in that swizzled layout.
+//  * MFMA operands must be K-contiguous; a weight given as [K, N] is first
+//    transposed to [N, K] in scratch by a tiled transpose launch.
+//  * Tiles are remapped so that consecutive workgroups of one XCD (the
+//    hardware deals workgroups round-robin over the 8 XCDs) take a compact
+//    group of tiles and share operand slices in that XCD's L2.
+//  * The epilogue stages 32-row slabs of accumulators through LDS so each
+//    lane finishes 8 consecutive columns and writes them with one 16-byte
+//    store.
 #include "dev.hpp"
+
 namespace mk {
-bool gemm_mfma_supported(int, const GemmArgs&) { return false; }
-hipError_t launch_gemm_mfma(int, const GemmArgs&, hipStream_t) { return hipErrorInvalidValue; }
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+namespace {
+
+constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int kStages = 4;
+constexpr int kTileBytes = BM * BK * 2;           // 16 KB per operand slice
+constexpr int kStageBytes = 2 * kTileBytes;       // 32 KB per stage
+constexpr int kGroupM = 8;                        // tile rows per locality group
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+// Byte offset of chunk c of row r inside a [rows][32] bf16 operand slice.
+__device__ __forceinline__ int lds_off(int r, int c) { return r * 64 + ((c ^ swz(r)) << 4); }
+
+__device__ __forceinline__ uint32_t dw(const uint4& v, int d) {
+  return d == 0 ? v.x : d == 1 ? v.y : d == 2 ? v.z : v.w;
 }
+
+struct TileCoord {
+  int tm, tn;
+};
+
+// Logical tile of this workgroup: XCD-aware remap, then grouped (column-major
+// within groups of kGroupM tile rows) order.
+__device__ __forceinline__ TileCoord tile_of(int bid, int tiles_m, int tiles_n) {
+  const int total = tiles_m * tiles_n;
+  if (total % kXcds == 0) bid = (bid % kXcds) * (total / kXcds) + bid / kXcds;
+  const int per_group = kGroupM * tiles_n;
+  const int g = bid / per_group;
+  const int first_m = g * kGroupM;
+  const int gsize = min(tiles_m - first_m, kGroupM);
+  const int r = bid % per_group;
+  return {first_m + r % gsize, r / gsize};
+}
+
+// Global operand access through buffer resources: a lane whose element lies
+// outside the operand gets an offset beyond the descriptor's range and reads
+// zeros, so ragged M / N / K tails need no branches.
+constexpr uint32_t kOob = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0));
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Direct HBM -> LDS loads of one operand slice (1024 16-byte chunks).  For
+// load q of wave w, lane i fills LDS chunk p = (q*WAVES + w)*64 + i, i.e. row
+// p/4, physical chunk p%4, whose logical chunk is (p%4) ^ swz(row).
+template <int WAVES>
+struct SliceLoader {
+  static constexpr int LQ = 16 / WAVES;   // loads per thread per operand slice
+  __amdgpu_buffer_rsrc_t src;
+  uint32_t voff[LQ];   // byte offset at k0 = 0, kOob if the row is out of range
+  int lchunk[LQ];      // logical 16-byte chunk of this lane's loads
+
+  __device__ __forceinline__ void init(const bf16* base, int64_t rows, int64_t ld, int64_t r0) {
+    src = make_rsrc(base, rows * ld * 2);
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+    for (int q = 0; q < LQ; ++q) {
+      const int p = (q * WAVES + w) * 64 + lane;
+      const int row = p >> 2;
+      const int c = (p & 3) ^ swz(row);
+      lchunk[q] = c;
+      const int64_t g = r0 + row;
+      voff[q] = g < rows ? (uint32_t)(g * ld * 2 + c * 16) : kOob;
+    }
+  }
+
+  // Issue the loads of the slice starting at k0 into `dst` (this operand's
+  // slice inside a stage).
+  __device__ __forceinline__ void issue(char* dst, int64_t k0, int64_t K) const {
+    const int w = threadIdx.x >> 6;
+    const int64_t krem = K - k0;
+#pragma unroll
+    for (int q = 0; q < LQ; ++q) {
+      const uint32_t off = lchunk[q] * 8 < krem ? voff[q] : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * WAVES + w) * 1024),
+                                               16, (int)off, (int)(k0 * 2), 0, 0);
+    }
+  }
+};
+
+// MFMA operand fragments of one 16-deep k step for this wave: 4 row tiles of
+// A and NJ column tiles of B (32 x 16 bf16 each).
+template <int NJ>
+struct Frags {
+  bf16x8 a[4], b[NJ];
+};
+
+template <int NJ>
+__device__ __forceinline__ void load_frags(const char* stage, int kk, int rowbase, int colbase,
+                                           int lr, int lh, Frags<NJ>& f) {
+  const char* la = stage;
+  const char* lb = stage + kTileBytes;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    f.a[i] = *(const bf16x8*)(la + lds_off(rowbase + i * 32 + lr, kk * 2 + lh));
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    f.b[j] = *(const bf16x8*)(lb + lds_off(colbase + j * 32 + lr, kk * 2 + lh));
+}
+
+template <int NJ>
+__device__ __forceinline__ void mfma_step(const Frags<NJ>& f, f32x16 (&acc)[4][NJ]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+}
+
+// vmcnt(n) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// Copy acc[I][j][r] (rows I*32 .. I*32+31 of this wave's tile) into the wave's
+// slab: element (row (r/4)*8 + lh*4 + r%4, column j*32 + lr), row stride LD.
+template <int I, int NJ, int LD>
+__device__ __forceinline__ void stage_slab(const f32x16 (&acc)[4][NJ], float* slab, int lh,
+                                           int lr) {
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      slab[((r >> 2) * 8 + lh * 4 + (r & 3)) * LD + j * 32 + lr] = acc[I][j][r];
+}
+
+// B is [N, K] (K contiguous) here; a [K, N] weight arrives pre-transposed.
+// WN waves along N (2: four waves of 128 x 128; 4: eight waves of 128 x 64,
+// two per SIMD so one wave's MFMAs cover the other's waits).
+template <int WN>
+__global__ __launch_bounds__(128 * WN, 1) void gemm_bf16_mfma_kernel(GemmArgs a) {
+  constexpr int WAVES = 2 * WN, THREADS = 64 * WAVES;
+  constexpr int WTN = BN / WN;        // wave tile columns
+  constexpr int NJ = WTN / 32;        // 32-wide column tiles per wave
+  constexpr int LD = WTN + 8;         // epilogue slab row stride (floats)
+  constexpr int LPR = WTN / 8;        // lanes per slab row in the epilogue
+  constexpr int RPP = 64 / LPR;       // slab rows per pass
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
+  const int tiles_m = (int)((a.M + BM - 1) / BM), tiles_n = (int)((a.N + BN - 1) / BN);
+  const TileCoord tc = tile_of(blockIdx.x, tiles_m, tiles_n);
+  const int64_t m0 = (int64_t)tc.tm * BM, n0 = (int64_t)tc.tn * BN;
+  const int64_t z = blockIdx.y, bb = z / a.heads, hh = z % a.heads;
+  const bf16* A = (const bf16*)a.A + a.a_off + bb * a.a_sb + hh * a.a_sh;
+  const bf16* B = (const bf16*)a.B + a.b_off + bb * a.b_sb + hh * a.b_sh;
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w / WN, wn = w % WN;
+  const int lr = lane & 31, lh = lane >> 5;
+  const int rowbase = wm * 128, colbase = wn * WTN;
+
+  f32x16 acc[4][NJ];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nk = (int)((a.K + BK - 1) / BK);
+  SliceLoader<WAVES> la, lb;
+  la.init(A, a.M, a.lda, m0);
+  lb.init(B, a.N, a.ldb, n0);
+#pragma unroll
+  for (int s = 0; s < kStages - 1; ++s)
+    if (s < nk) {
+      la.issue(smem + s * kStageBytes, (int64_t)s * BK, a.K);
+      lb.issue(smem + s * kStageBytes + kTileBytes, (int64_t)s * BK, a.K);
+    }
+
+  constexpr int LPS = 2 * (16 / WAVES);   // loads per thread per slice
+  for (int kt = 0; kt < nk; ++kt) {
+    // Slice kt has landed once at most the loads of the (up to two) later
+    // slices are outstanding.
+    const int later = min(kStages - 2, nk - 1 - kt);
+    if (later >= 2)
+      wait_vm<2 * LPS>();
+    else if (later == 1)
+      wait_vm<LPS>();
+    else
+      wait_vm<0>();
+    // A bare barrier: __syncthreads() would also drain every outstanding load
+    // (its fence), which defeats the ring.  The slice's own loads are complete
+    // (vmcnt above), and fragment reads of the slot about to be refilled were
+    // consumed by MFMAs before this point.
+    __builtin_amdgcn_s_barrier();
+    const int nxt = kt + kStages - 1;
+    if (nxt < nk) {
+      char* st = smem + (nxt % kStages) * kStageBytes;
+      la.issue(st, (int64_t)nxt * BK, a.K);
+      lb.issue(st + kTileBytes, (int64_t)nxt * BK, a.K);
+    }
+    const char* cur = smem + (kt % kStages) * kStageBytes;
+    Frags<NJ> f0, f1;
+    load_frags<NJ>(cur, 0, rowbase, colbase, lr, lh, f0);
+    load_frags<NJ>(cur, 1, rowbase, colbase, lr, lh, f1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step<NJ>(f0, acc);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step<NJ>(f1, acc);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // ---------------------------------------------------------------- epilogue
+  // acc[i][j][r] is C[row, col] with
+  //   row = m0 + rowbase + i*32 + (r/4)*8 + lh*4 + r%4,  col = n0 + colbase + j*32 + lr.
+  // Each wave stages one 32-row slab at a time in its own LDS region, then
+  // every lane applies the chain to 8 consecutive columns and writes them with
+  // one 16-byte store.
+  wait_vm<0>();
+  __syncthreads();   // operand slices are dead; reuse LDS
+  float* slab = (float*)smem + w * (32 * LD);
+  float* red = (float*)smem + WAVES * 32 * LD;   // [WN column groups][256 rows][2]
+  const int64_t cbase = a.c_off + bb * a.c_sb + hh * a.c_sh;
+  bf16* C = (bf16*)a.C + cbase;
+  const bool softmax = a.terminal == TERM_SOFTMAX;
+  const int q = lane % LPR;          // 8-column group within the slab row
+  const int64_t col0 = n0 + colbase + q * 8;
+  // 16-byte accesses to C and to residual operands need 8-aligned offsets.
+  const bool vec_ok = ((a.ldc | cbase) & 7) == 0;
+  const int valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
+
+  auto finish_slab = [&](int i) {
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): slab writes done (wave-private)
+    __builtin_amdgcn_wave_barrier();
+    for (int pass = 0; pass < 32 / RPP; ++pass) {
+      const int rl = pass * RPP + lane / LPR;
+      const int lrow = rowbase + i * 32 + rl;
+      const int64_t row = m0 + lrow;
+      const float4 lo = *(const float4*)(slab + rl * LD + q * 8);
+      const float4 hi = *(const float4*)(slab + rl * LD + q * 8 + 4);
+      float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      const bool row_ok = row < a.M;
+      float m = -INFINITY, sum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] *= a.alpha;
+      if (a.epi.n && row_ok && valid > 0)
+        epi_apply8<bf16>(a.epi, v, row, col0, valid, cbase + row * a.ldc + col0,
+                         valid == 8 && vec_ok);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (a.terminal != TERM_ROWSUM) v[e] = bf2f(f2bf(v[e]));
+        if (e < valid) {
+          m = fmaxf(m, v[e]);
+          sum += v[e];
+        }
+      }
+      if (a.terminal != TERM_ROWSUM && row_ok) {
+        if (valid == 8) {
+          uint4 o;
+          o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+          o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+          o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
+          o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+          if (vec_ok) {
+            *(uint4*)(C + row * a.ldc + col0) = o;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) C[row * a.ldc + col0 + e] = f2bf(v[e]);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (e < valid) C[row * a.ldc + col0 + e] = f2bf(v[e]);
+        }
+      }
+      if (a.terminal != TERM_NONE) {
+        // reduce over the LPR lanes that share this row (this wave's columns)
+        if (softmax) {
+#pragma unroll
+          for (int o = LPR / 2; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+          sum = 0.f;
+          if (m != -INFINITY) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (e < valid) sum += __expf(v[e] - m);
+          }
+        }
+#pragma unroll
+        for (int o = LPR / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
+        if (q == 0) {
+          red[(wn * 256 + lrow) * 2] = m;
+          red[(wn * 256 + lrow) * 2 + 1] = sum;
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  };
+  // A switch keeps every acc index static while the finishing code exists
+  // once (the loop itself is not unrolled).
+  for (int i = 0; i < 4; ++i) {
+    switch (i) {
+      case 0: stage_slab<0, NJ, LD>(acc, slab, lh, lr); break;
+      case 1: stage_slab<1, NJ, LD>(acc, slab, lh, lr); break;
+      case 2: stage_slab<2, NJ, LD>(acc, slab, lh, lr); break;
+      default: stage_slab<3, NJ, LD>(acc, slab, lh, lr); break;
+    }
+    finish_slab(i);
+  }
+  if (a.terminal == TERM_NONE) return;
+  __syncthreads();
+  for (int lrow = threadIdx.x; lrow < BM; lrow += THREADS) {
+    const int64_t row = m0 + lrow;
+    if (row >= a.M) break;
+    float* part = a.partial + (row * a.n_tiles + tc.tn) * (softmax ? 2 : 1);
+    if (softmax) {
+      float mm = -INFINITY;
+#pragma unroll
+      for (int g = 0; g < WN; ++g) mm = fmaxf(mm, red[(g * 256 + lrow) * 2]);
+      float ss = 0.f;
+      if (mm != -INFINITY) {
+#pragma unroll
+        for (int g = 0; g < WN; ++g) {
+          const float mg = red[(g * 256 + lrow) * 2];
+          if (mg != -INFINITY) ss += red[(g * 256 + lrow) * 2 + 1] * __expf(mg - mm);
+        }
+      }
+      part[0] = mm;
+      part[1] = ss;
+    } else {
+      float ss = 0.f;
+#pragma unroll
+      for (int g = 0; g < WN; ++g) ss += red[(g * 256 + lrow) * 2 + 1];
+      part[0] = ss;
+    }
+  }
+}
+
+// B(k, n) of a [K, N] operand (batched) -> dst[z][n][k], K contiguous.  One
+// 64 x 64 tile per workgroup through LDS; 16-byte global accesses on both
+// sides (K and N are multiples of 8).
+__global__ __launch_bounds__(256) void transpose_b_kernel(GemmArgs a, bf16* dst) {
+  __shared__ bf16 tile[64][72];
+  const int64_t z = blockIdx.z, bb = z / a.heads, hh = z % a.heads;
+  const bf16* src = (const bf16*)a.B + a.b_off + bb * a.b_sb + hh * a.b_sh;
+  const int64_t k0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
+  const int t = threadIdx.x, r = t >> 3, c8 = (t & 7) * 8;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int64_t k = k0 + r + h * 32, n = n0 + c8;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (k < a.K && n < a.N) v = *(const uint4*)(src + k * a.ldb + n);
+    *(uint4*)&tile[r + h * 32][c8] = v;
+  }
+  __syncthreads();
+  bf16* out = dst + z * a.N * a.K;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int nl = r + h * 32;
+    const int64_t n = n0 + nl, k = k0 + c8;
+    if (n < a.N && k < a.K) {
+      uint4 v;
+      v.x = (uint32_t)tile[c8 + 0][nl] | ((uint32_t)tile[c8 + 1][nl] << 16);
+      v.y = (uint32_t)tile[c8 + 2][nl] | ((uint32_t)tile[c8 + 3][nl] << 16);
+      v.z = (uint32_t)tile[c8 + 4][nl] | ((uint32_t)tile[c8 + 5][nl] << 16);
+      v.w = (uint32_t)tile[c8 + 6][nl] | ((uint32_t)tile[c8 + 7][nl] << 16);
+      *(uint4*)(out + n * a.K + k) = v;
+    }
+  }
+}
+
+}  // namespace
+
+bool gemm_mfma_supported(int dtype, const GemmArgs& a) {
+  if (dtype != MK_BF16) return false;
+  // 16-byte operand chunks: K (and N for a [K, N] weight), leading dimensions
+  // and batch offsets must be multiples of 8 elements.
+  if (a.K % 8 || a.lda % 8 || a.ldb % 8) return false;
+  if (a.layout == 1 && a.N % 8) return false;
+  const int64_t offs[] = {a.a_off, a.a_sb, a.a_sh, a.b_off, a.b_sb, a.b_sh};
+  for (int64_t o : offs)
+    if (o % 8) return false;
+  if (a.M < 1 || a.N < 1 || a.K < 1) return false;
+  if (a.terminal != TERM_NONE && a.batch * a.heads != 1) return false;
+  // Buffer-resource ranges are 32-bit: every operand slice must stay below 2 GB.
+  const int64_t lim = (int64_t)1 << 31;
+  if (a.M * a.lda * 2 >= lim || a.N * (a.layout == 0 ? a.ldb : a.K) * 2 >= lim) return false;
+  const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  return tiles < (1ll << 31) && a.batch * a.heads <= 65535;
+}
+
+int64_t gemm_mfma_bt_bytes(const GemmArgs& a) {
+  return a.layout == 1 ? (int64_t)a.batch * a.heads * a.N * a.K * 2 : 0;
+}
+
+hipError_t launch_transpose_b(const GemmArgs& a, void* dst, hipStream_t st) {
+  dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)((a.K + 63) / 64),
+            (unsigned)(a.batch * a.heads));
+  hipLaunchKernelGGL(transpose_b_kernel, grid, dim3(256), 0, st, a, (bf16*)dst);
+  return hipGetLastError();
+}
+
+GemmArgs gemm_with_bt(const GemmArgs& a, const void* bt) {
+  GemmArgs g = a;
+  g.B = bt;
+  g.layout = 0;
+  g.ldb = a.K;
+  g.b_off = 0;
+  g.b_sh = a.N * a.K;
+  g.b_sb = (int64_t)a.heads * a.N * a.K;
+  return g;
+}
+
+hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
+  if (!gemm_mfma_supported(dtype, a) || a.layout != 0) return hipErrorInvalidValue;
+  if (((uintptr_t)a.A | (uintptr_t)a.B) % 16) return hipErrorInvalidValue;
+  const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  dim3 grid((unsigned)tiles, (unsigned)(a.batch * a.heads));
+  // Eight waves (two per SIMD) measured faster than four on every workload.
+  hipLaunchKernelGGL(gemm_bf16_mfma_kernel<4>, grid, dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace mk

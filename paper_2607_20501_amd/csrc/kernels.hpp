@@ -88,6 +88,12 @@ hipError_t launch_attn_simple(int dtype, const AttnArgs& a, hipStream_t st);
 // Tuned kernels.
 constexpr int64_t kMfmaTileN = 256;   // column tile of the bf16 MFMA GEMM
 bool gemm_mfma_supported(int dtype, const GemmArgs& a);
+// The MFMA kernel takes B as [N, K]; a [K, N] operand (layout 1) is first
+// transposed into scratch of gemm_mfma_bt_bytes() bytes, and gemm_with_bt()
+// gives the arguments that read it there.
+int64_t gemm_mfma_bt_bytes(const GemmArgs& a);
+hipError_t launch_transpose_b(const GemmArgs& a, void* dst, hipStream_t st);
+GemmArgs gemm_with_bt(const GemmArgs& a, const void* bt);
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st);
 
 }  // namespace mk

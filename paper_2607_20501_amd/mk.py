@@ -81,7 +81,7 @@ class mk_verify_report(ctypes.Structure):
 
 EXPORTS = ["mk_decomposition_preset", "mk_module_create", "mk_module_destroy", "mk_module_info",
            "mk_subkernel_info", "mk_subkernel_select", "mk_workspace_size", "mk_run",
-           "mk_verify", "mk_status_str", "mk_last_error"]
+           "mk_verify", "mk_status_str", "mk_last_error", "mk_profile_begin", "mk_profile_end"]
 
 _lib = None
 
@@ -111,6 +111,10 @@ def load():
               "mk_subkernel_info", "mk_subkernel_select", "mk_workspace_size", "mk_run",
               "mk_verify"):
         getattr(lib, f).restype = ctypes.c_int
+    lib.mk_profile_begin.argtypes = [vp, ctypes.c_int32]
+    lib.mk_profile_end.argtypes = [vp, P(ctypes.c_float), ctypes.c_int32, P(ctypes.c_int32)]
+    lib.mk_profile_begin.restype = ctypes.c_int
+    lib.mk_profile_end.restype = ctypes.c_int
     lib.mk_status_str.argtypes = [ctypes.c_int]
     lib.mk_status_str.restype = ctypes.c_char_p
     lib.mk_last_error.argtypes = []
@@ -209,6 +213,18 @@ def mk_run(h, dev_inputs, dev_out, dev_ws, ws_bytes, stream, n_subkernels=None):
     return list(ms) if ms is not None else None
 
 
+def mk_profile_begin(h, max_launches):
+    _check(load().mk_profile_begin(h, int(max_launches)))
+
+
+def mk_profile_end(h, capacity):
+    """Returns the list of recorded per-launch milliseconds."""
+    buf = (ctypes.c_float * max(1, capacity))()
+    n = ctypes.c_int32()
+    _check(load().mk_profile_end(h, buf, int(capacity), ctypes.byref(n)))
+    return list(buf[:min(n.value, capacity)])
+
+
 def mk_verify(h, dev_inputs, dev_out, dev_ws, ws_bytes, stream, checks):
     """checks: list of dicts {stage, expect (float64 array), index (int64 array
     or None), rtol, atol}.  Returns the report as a dict."""
@@ -274,6 +290,15 @@ class Module:
 
     def workspace_size(self):
         return mk_workspace_size(self.h)
+
+    def launches_per_run(self):
+        return sum(s["n_launches"] for s in self.subkernels())
+
+    def profile_begin(self, max_launches):
+        mk_profile_begin(self.h, max_launches)
+
+    def profile_end(self, capacity):
+        return mk_profile_end(self.h, capacity)
 
     @staticmethod
     def _ptrs(tensors):
