@@ -292,7 +292,13 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       a.B = t.B; a.H = t.H; a.dh = t.dh; a.S = t.S;
       a.scale = t.scale;
       a.causal = t.causal ? (impl == MUT_MASK_OFF_BY_ONE ? 2 : 1) : 0;
-      return hip_check(timed([&] { return launch_attn_simple(dt, a, st); }), "attention");
+      const bool fused = impl != MK_IMPL_SIMPLE && attn_fused_supported(dt, a) &&
+                         (uintptr_t)a.qkv % 16 == 0 && (uintptr_t)a.o % 16 == 0;
+      return hip_check(timed([&] {
+                         return fused ? launch_attn_fused(dt, a, st)
+                                      : launch_attn_simple(dt, a, st);
+                       }),
+                       "attention");
     }
     default:
       return fail(MK_E_INTERNAL, "unknown family");

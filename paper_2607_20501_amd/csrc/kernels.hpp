@@ -95,5 +95,7 @@ int64_t gemm_mfma_bt_bytes(const GemmArgs& a);
 hipError_t launch_transpose_b(const GemmArgs& a, void* dst, hipStream_t st);
 GemmArgs gemm_with_bt(const GemmArgs& a, const void* bt);
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st);
+bool attn_fused_supported(int dtype, const AttnArgs& a);
+hipError_t launch_attn_fused(int dtype, const AttnArgs& a, hipStream_t st);
 
 }  // namespace mk
