@@ -13,6 +13,7 @@ live over the timed steps) and the oracle's CPU throughput on a bounded row
 sample (which also checks those rows of the GPU output).
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -40,19 +41,53 @@ def build_module(cfg, dtype):
 
 
 def launch_names(mod):
-    """Name of every kernel launch of one run, in order."""
+    """Name of every kernel launch of one run, in order.  A GEMM subkernel runs
+    [layernorm prologue] [transpose of a [K,N] weight] gemm [row finisher]."""
     names = []
     for s in mod.subkernels():
         ops = [o["kind"] for o in mod.desc["ops"][s["op_begin"]:s["op_end"]]]
+        n = s["n_launches"]
         if s["family"] == "GEMM":
-            seq = ["layernorm prologue (row_kernel)"] if ops[0] == "LAYERNORM" else []
-            seq.append("gemm_bf16_mfma_kernel (fused epilogue: " + ",".join(ops) + ")")
-            if ops[-1] in ("SOFTMAX", "ROWSUM"):
+            ln = ops[0] == "LAYERNORM"
+            fin = ops[-1] in ("SOFTMAX", "ROWSUM")
+            seq = ["row_kernel (layernorm prologue)"] if ln else []
+            if n - len(seq) - (2 if fin else 1) == 1:
+                seq.append("transpose_b_kernel")
+            seq.append("gemm_bf16_mfma_kernel (" + ",".join(ops) + ")")
+            if fin:
                 seq.append(ops[-1].lower() + "_finish_kernel")
-            names += seq[:s["n_launches"]] + ["?"] * (s["n_launches"] - len(seq))
+            names += seq
+        elif s["family"] == "ATTN":
+            names += ["attn_fwd_kernel (" + ",".join(ops) + ")"] * n
         else:
-            names += [s["family"].lower() + " subkernel (" + ",".join(ops) + ")"] * s["n_launches"]
+            names += [s["family"].lower() + " subkernel (" + ",".join(ops) + ")"] * n
     return names
+
+
+def source_digest(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+GEMM_SOURCES = ["paper_2607_20501_amd/csrc/k_gemm_mfma.hip", "paper_2607_20501_amd/csrc/dev.hpp",
+                "paper_2607_20501_amd/csrc/kernels.hpp", "paper_2607_20501_amd/csrc/plan_codes.hpp"]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    counter summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        table = json.load(fh)
+    rec = table.get(workload, {}).get(kernel)
+    if not rec or rec.get("source_digest") != source_digest(GEMM_SOURCES):
+        return None
+    return rec["hbm_bytes_per_launch"]
 
 
 def time_module(mod, ins, out, ws, steps, warmup):
@@ -114,7 +149,9 @@ def main():
     ap.add_argument("--decomp", default="fused", choices=["fused", "split"])
     ap.add_argument("--no-split", action="store_true", help="skip timing the split form")
     ap.add_argument("--cpu-rows", type=int, default=None,
-                    help="rows of the oracle sample (default: about 30 GFLOP of work)")
+                    help="rows of the oracle sample (default: about 300 GFLOP of work)")
+    ap.add_argument("--calibration-copy-mb", type=int, default=0,
+                    help="run one plain device copy of this size first (counter calibration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     args = ap.parse_args()
@@ -138,6 +175,15 @@ def main():
     ins, _, ws = mk.device_buffers(module, host, ws_bytes)
     out = mk.out_tensor(module, fused.info["out_shape"])
     flops = fused.info["flops"]
+    if args.calibration_copy_mb:
+        n = args.calibration_copy_mb << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {n} bytes")
+        del src, dst
 
     ms, per_launch = time_module(fused, ins, out, ws, args.steps, args.warmup)
     log(f"{args.decomp}: {ms * 1e3:.1f} us/step, launches (us): "
@@ -165,7 +211,8 @@ def main():
         achieved = sub["flops"] / (per_launch[k] * 1e-3) / 1e12
         peak = PEAK_BF16_TFLOPS if bf else PEAK_F32_TFLOPS
         roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                "frac": achieved / peak, "traffic": None}
+                "frac": achieved / peak,
+                "traffic": measured_traffic(module["name"], names[k].split(" ")[0])}
     else:
         achieved = sub["alg_bytes"] / (per_launch[k] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -197,7 +244,7 @@ def main():
     line.update(result)
     if not args.no_cpu_baseline and args.config in (1, 2, 4):
         M = module["inputs"][0][0]
-        rows = args.cpu_rows or max(1, min(M, int(30e9 / (flops / M))))
+        rows = args.cpu_rows or max(1, min(M, int(300e9 / (flops / M))))
         line["cpu_baseline"] = cpu_baseline(module, host, rows, out)
     print(json.dumps(line), flush=True)
 
