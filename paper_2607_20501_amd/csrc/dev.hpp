@@ -120,7 +120,8 @@ __device__ __forceinline__ void ld8(const T* p, bool vec, int valid, float (&out
 // `vec` says that 16-byte operand accesses are aligned and in range.
 template <typename T>
 __device__ __forceinline__ void epi_apply8(const EpiDev& e, float (&v)[8], int64_t row,
-                                           int64_t col0, int valid, int64_t flat0, bool vec) {
+                                           int64_t col0, int64_t ch, int valid, int64_t flat0,
+                                           bool vec) {
 #pragma unroll
   for (int i = 0; i < kMaxEpi; ++i) {
     if (i >= e.n) break;
@@ -136,6 +137,12 @@ __device__ __forceinline__ void epi_apply8(const EpiDev& e, float (&v)[8], int64
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] += t[k];
         break;
+      case EPI_BIAS_CH: {
+        const float bch = ld<T>((const T*)e.ptr[i], ch);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] += bch;
+        break;
+      }
       case EPI_RELU:
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] = fmaxf(v[k], 0.0f);

@@ -107,7 +107,25 @@ static GemmScratch gemm_scratch(const Plan& p, const Subkernel& sk, int impl) {
   return s;
 }
 
+static ConvArgs conv_args(const ConvSpec& c) {
+  ConvArgs a{};
+  a.N = c.N; a.C = c.C; a.H = c.H; a.W = c.W; a.K = c.K; a.R = c.R; a.S = c.S;
+  a.P = c.P; a.Q = c.Q; a.stride = c.stride; a.pad = c.pad;
+  a.gap = c.gap ? 1 : 0;
+  return a;
+}
+
+static bool use_conv_mfma(const Plan& p, const Subkernel& sk, int impl) {
+  return impl != MK_IMPL_SIMPLE && sk.family == MK_FAM_CONV &&
+         conv_mfma_supported(p.dtype, conv_args(sk.conv));
+}
+
 int64_t impl_scratch(const Plan& p, const Subkernel& sk, int impl) {
+  if (sk.family == MK_FAM_CONV) {
+    if (!use_conv_mfma(p, sk, impl)) return 0;
+    const ConvScratch c = conv_mfma_scratch(conv_args(sk.conv));
+    return c.xp_bytes + c.wp_bytes + c.partial_bytes;
+  }
   if (sk.family != MK_FAM_GEMM) return 0;
   const GemmScratch s = gemm_scratch(p, sk, impl);
   return s.ln_bytes + s.bt_bytes + s.partial_bytes;
@@ -123,6 +141,7 @@ int impl_launches(const Plan& p, const Subkernel& sk, int impl) {
     return 1 + (sk.gemm.ln ? 1 : 0) + (transpose ? 1 : 0) +
            (sk.gemm.terminal != TERM_NONE ? 1 : 0);
   }
+  if (sk.family == MK_FAM_CONV && use_conv_mfma(p, sk, impl)) return sk.conv.gap ? 4 : 3;
   return 1;
 }
 
@@ -274,15 +293,27 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
     }
     case MK_FAM_CONV: {
       const ConvSpec& c = sk.conv;
-      ConvArgs a{};
+      ConvArgs a = conv_args(c);
       a.x = vals[c.x_value];
       a.w = vals[c.w_value];
       a.y = out;
-      a.N = c.N; a.C = c.C; a.H = c.H; a.W = c.W; a.K = c.K; a.R = c.R; a.S = c.S;
-      a.P = c.P; a.Q = c.Q; a.stride = c.stride; a.pad = c.pad;
       a.epi = resolve(c.epi, vals, impl);
-      a.gap = c.gap ? 1 : 0;
-      return hip_check(timed([&] { return launch_conv_simple(dt, a, st); }), "conv");
+      if (!use_conv_mfma(p, sk, impl))
+        return hip_check(timed([&] { return launch_conv_simple(dt, a, st); }), "conv");
+      // Implicit GEMM: repack input and weights into scratch, run the MFMA
+      // GEMM in conv mode, then (GAP) combine the per-tile partials.
+      const ConvScratch cs = conv_mfma_scratch(a);
+      char* xp = (char*)scratch;
+      char* wp = xp + cs.xp_bytes;
+      float* part = (float*)(wp + cs.wp_bytes);
+      mk_status s = hip_check(timed([&] { return launch_pack_nhwc(a, xp, st); }), "pack nhwc");
+      if (s != MK_OK) return s;
+      s = hip_check(timed([&] { return launch_pack_krsc(a, wp, st); }), "pack krsc");
+      if (s != MK_OK) return s;
+      const GemmArgs g = conv_gemm_args(a, xp, wp, part);
+      s = hip_check(timed([&] { return launch_gemm_mfma(dt, g, st); }), "conv gemm");
+      if (s != MK_OK || !a.gap) return s;
+      return hip_check(timed([&] { return launch_gap_finish(a, part, st); }), "gap finish");
     }
     case MK_FAM_ATTN: {
       const AttnSpec& t = sk.attn;

@@ -112,17 +112,38 @@ struct SliceLoader {
     }
   }
 
+  // Rows gathered from arbitrary byte offsets (implicit-GEMM conv: output
+  // position m -> its window origin in the padded NHWC input).
+  template <typename RowOff>
+  __device__ __forceinline__ void init_gather(const bf16* base, int64_t bytes, int64_t rows,
+                                              int64_t r0, RowOff rowoff) {
+    src = make_rsrc(base, bytes);
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+    for (int q = 0; q < LQ; ++q) {
+      const int p = (q * WAVES + w) * 64 + lane;
+      const int row = p >> 2;
+      const int c = (p & 3) ^ swz(row);
+      lchunk[q] = c;
+      const int64_t g = r0 + row;
+      voff[q] = g < rows ? (uint32_t)(rowoff(g) + c * 16) : kOob;
+    }
+  }
+
   // Issue the loads of the slice starting at k0 into `dst` (this operand's
-  // slice inside a stage).
-  __device__ __forceinline__ void issue(char* dst, int64_t k0, int64_t K) const {
+  // slice inside a stage); `soff` is the slice's byte offset along K.
+  __device__ __forceinline__ void issue(char* dst, int64_t k0, int64_t K, uint32_t soff) const {
     const int w = threadIdx.x >> 6;
     const int64_t krem = K - k0;
 #pragma unroll
     for (int q = 0; q < LQ; ++q) {
       const uint32_t off = lchunk[q] * 8 < krem ? voff[q] : kOob;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * WAVES + w) * 1024),
-                                               16, (int)off, (int)(k0 * 2), 0, 0);
+                                               16, (int)off, (int)soff, 0, 0);
     }
+  }
+  __device__ __forceinline__ void issue(char* dst, int64_t k0, int64_t K) const {
+    issue(dst, k0, K, (uint32_t)(k0 * 2));
   }
 };
 
@@ -176,7 +197,15 @@ __device__ __forceinline__ void stage_slab(const f32x16 (&acc)[4][NJ], float* sl
 // B is [N, K] (K contiguous) here; a [K, N] weight arrives pre-transposed.
 // WN waves along N (2: four waves of 128 x 128; 4: eight waves of 128 x 64,
 // two per SIMD so one wave's MFMAs cover the other's waits).
-template <int WN>
+// Byte offset along K of implicit-GEMM slice k0 (k = (r*S + s)*C + c, and a
+// 32-deep slice never crosses an (r, s) boundary since C % 32 == 0).
+__device__ __forceinline__ uint32_t conv_koff(const GemmArgs& a, int64_t k0) {
+  const int64_t rs = k0 / a.cv_C, c0 = k0 % a.cv_C;
+  const int64_t r = rs / a.cv_S, s = rs % a.cv_S;
+  return (uint32_t)(((r * a.cv_Wp + s) * a.cv_C + c0) * 2);
+}
+
+template <int WN, int CONV>
 __global__ __launch_bounds__(128 * WN, 1) void gemm_bf16_mfma_kernel(GemmArgs a) {
   constexpr int WAVES = 2 * WN, THREADS = 64 * WAVES;
   constexpr int WTN = BN / WN;        // wave tile columns
@@ -208,12 +237,28 @@ __global__ __launch_bounds__(128 * WN, 1) void gemm_bf16_mfma_kernel(GemmArgs a)
   const int nk = (int)((a.K + BK - 1) / BK);
   SliceLoader<WAVES> la, lb;
   la.init(A, a.M, a.lda, m0);
-  lb.init(B, a.N, a.ldb, n0);
+  const int64_t PQ = a.cv_P * a.cv_Q;
+  if (CONV) {
+    const int64_t bytes = a.cv_Hp * a.cv_Wp * a.cv_C * 2 * (a.N / PQ);
+    lb.init_gather(B, bytes, a.N, n0, [&](int64_t m) {
+      const int64_t n = m / PQ, pq = m % PQ;
+      const int64_t p = pq / a.cv_Q, q = pq % a.cv_Q;
+      return ((n * a.cv_Hp + p * a.cv_stride) * a.cv_Wp + q * a.cv_stride) * a.cv_C * 2;
+    });
+  } else {
+    lb.init(B, a.N, a.ldb, n0);
+  }
+  auto issue_b = [&](char* dst, int64_t k0) {
+    if (CONV)
+      lb.issue(dst, k0, a.K, conv_koff(a, k0));
+    else
+      lb.issue(dst, k0, a.K);
+  };
 #pragma unroll
   for (int s = 0; s < kStages - 1; ++s)
     if (s < nk) {
       la.issue(smem + s * kStageBytes, (int64_t)s * BK, a.K);
-      lb.issue(smem + s * kStageBytes + kTileBytes, (int64_t)s * BK, a.K);
+      issue_b(smem + s * kStageBytes + kTileBytes, (int64_t)s * BK);
     }
 
   constexpr int LPS = 2 * (16 / WAVES);   // loads per thread per slice
@@ -236,7 +281,7 @@ __global__ __launch_bounds__(128 * WN, 1) void gemm_bf16_mfma_kernel(GemmArgs a)
     if (nxt < nk) {
       char* st = smem + (nxt % kStages) * kStageBytes;
       la.issue(st, (int64_t)nxt * BK, a.K);
-      lb.issue(st + kTileBytes, (int64_t)nxt * BK, a.K);
+      issue_b(st + kTileBytes, (int64_t)nxt * BK);
     }
     const char* cur = smem + (kt % kStages) * kStageBytes;
     Frags<NJ> f0, f1;
@@ -282,19 +327,59 @@ __global__ __launch_bounds__(128 * WN, 1) void gemm_bf16_mfma_kernel(GemmArgs a)
       float m = -INFINITY, sum = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] *= a.alpha;
+      // Offset of (row, col0) in the output: row-major, or NCHW for a conv
+      // (row = channel, col = position; PQ % 8 == 0 keeps the 8 in one image).
+      const int64_t img = CONV ? col0 / PQ : 0;
+      const int64_t obase = CONV ? (img * a.M + row) * PQ + (col0 - img * PQ)
+                                 : cbase + row * a.ldc + col0;
       if (a.epi.n && row_ok && valid > 0)
-        epi_apply8<bf16>(a.epi, v, row, col0, valid, cbase + row * a.ldc + col0,
-                         valid == 8 && vec_ok);
+        epi_apply8<bf16>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok));
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        if (a.terminal != TERM_ROWSUM) v[e] = bf2f(f2bf(v[e]));
+        if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX) v[e] = bf2f(f2bf(v[e]));
         if (e < valid) {
           m = fmaxf(m, v[e]);
           sum += v[e];
         }
       }
+      if (CONV && a.terminal == TERM_GAP) {
+        // Sum this lane's 8 positions into the slot of their image (the tile
+        // covers at most two images), then over the lanes sharing the row.
+        const int64_t img0 = (n0 < a.N ? n0 : a.N - 1) / PQ;
+        const bool second = row_ok && valid > 0 && img != img0;
+        float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e < valid) {
+            if (second) s1 += v[e];
+            else s0 += v[e];
+          }
+#pragma unroll
+        for (int o = LPR / 2; o > 0; o >>= 1) {
+          s0 += __shfl_xor(s0, o, 64);
+          s1 += __shfl_xor(s1, o, 64);
+        }
+        if (q == 0) {
+          red[(wn * 256 + lrow) * 2] = s0;
+          red[(wn * 256 + lrow) * 2 + 1] = s1;
+        }
+        continue;
+      }
       if (a.terminal != TERM_ROWSUM && row_ok) {
-        if (valid == 8) {
+        if (CONV) {
+          if (valid == 8) {
+            uint4 o;
+            o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+            o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+            o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
+            o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+            *(uint4*)(C + obase) = o;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (e < valid) C[obase + e] = f2bf(v[e]);
+          }
+        } else if (valid == 8) {
           uint4 o;
           o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
           o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
@@ -350,6 +435,16 @@ __global__ __launch_bounds__(128 * WN, 1) void gemm_bf16_mfma_kernel(GemmArgs a)
   for (int lrow = threadIdx.x; lrow < BM; lrow += THREADS) {
     const int64_t row = m0 + lrow;
     if (row >= a.M) break;
+    if (CONV) {   // GAP partials of this position tile, per image slot
+#pragma unroll
+      for (int slot = 0; slot < 2; ++slot) {
+        float ss = 0.f;
+#pragma unroll
+        for (int g = 0; g < WN; ++g) ss += red[(g * 256 + lrow) * 2 + slot];
+        a.partial[((int64_t)tc.tn * 2 + slot) * a.M + row] = ss;
+      }
+      continue;
+    }
     float* part = a.partial + (row * a.n_tiles + tc.tn) * (softmax ? 2 : 1);
     if (softmax) {
       float mm = -INFINITY;
@@ -450,12 +545,20 @@ GemmArgs gemm_with_bt(const GemmArgs& a, const void* bt) {
 }
 
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
-  if (!gemm_mfma_supported(dtype, a) || a.layout != 0) return hipErrorInvalidValue;
+  if (a.conv) {
+    if (dtype != MK_BF16 || a.cv_C % 32 || (a.cv_P * a.cv_Q) % 8 || a.lda % 8 || a.K % 32)
+      return hipErrorInvalidValue;
+  } else if (!gemm_mfma_supported(dtype, a) || a.layout != 0) {
+    return hipErrorInvalidValue;
+  }
   if (((uintptr_t)a.A | (uintptr_t)a.B) % 16) return hipErrorInvalidValue;
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   dim3 grid((unsigned)tiles, (unsigned)(a.batch * a.heads));
   // Eight waves (two per SIMD) measured faster than four on every workload.
-  hipLaunchKernelGGL(gemm_bf16_mfma_kernel<4>, grid, dim3(512), 0, st, a);
+  if (a.conv)
+    hipLaunchKernelGGL((gemm_bf16_mfma_kernel<4, 1>), grid, dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL((gemm_bf16_mfma_kernel<4, 0>), grid, dim3(512), 0, st, a);
   return hipGetLastError();
 }
 

@@ -50,6 +50,13 @@ struct GemmArgs {
   EpiDev epi;
   float* partial;          // row partials of the terminal reduction
   int64_t n_tiles;         // column tiles per row in `partial`
+  // Implicit-GEMM convolution (conv != 0): rows of A are output channels
+  // (weights repacked as [K][R][S][C]), columns are output positions
+  // m = (n, p, q) whose B rows are gathered from a zero-padded NHWC copy of the
+  // input; C is written NCHW, or reduced to per-tile GAP partials
+  // (terminal == TERM_GAP: partial[(tile * 2 + slot) * M + k]).
+  int32_t conv;
+  int64_t cv_C, cv_Hp, cv_Wp, cv_P, cv_Q, cv_S, cv_stride;
 };
 
 struct ConvArgs {
@@ -95,6 +102,18 @@ int64_t gemm_mfma_bt_bytes(const GemmArgs& a);
 hipError_t launch_transpose_b(const GemmArgs& a, void* dst, hipStream_t st);
 GemmArgs gemm_with_bt(const GemmArgs& a, const void* bt);
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st);
+// Implicit-GEMM conv: pack_nhwc (x -> zero-padded NHWC), pack_krsc (w ->
+// [K][R][S][C]), the GEMM kernel in conv mode, and for a fused GAP the
+// finisher over per-tile partials.
+struct ConvScratch {
+  int64_t xp_bytes, wp_bytes, partial_bytes;
+};
+bool conv_mfma_supported(int dtype, const ConvArgs& a);
+ConvScratch conv_mfma_scratch(const ConvArgs& a);
+hipError_t launch_pack_nhwc(const ConvArgs& a, void* xp, hipStream_t st);
+hipError_t launch_pack_krsc(const ConvArgs& a, void* wp, hipStream_t st);
+GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float* partial);
+hipError_t launch_gap_finish(const ConvArgs& a, const float* partial, hipStream_t st);
 bool attn_fused_supported(int dtype, const AttnArgs& a);
 hipError_t launch_attn_fused(int dtype, const AttnArgs& a, hipStream_t st);
 
