@@ -42,14 +42,15 @@ template <> __device__ __forceinline__ float rnd<bf16>(float v) { return bf2f(f2
 // t = 1 / (1 + p x) for x >= 0 (|error| <= 1.5e-7), odd extension for x < 0.
 __device__ __forceinline__ float erf_as(float x) {
   const float ax = fabsf(x);
-  const float t = __frcp_rn(1.0f + 0.3275911f * ax);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
   float poly = 1.061405429f;
   poly = fmaf(poly, t, -1.453152027f);
   poly = fmaf(poly, t, 1.421413741f);
   poly = fmaf(poly, t, -0.284496736f);
   poly = fmaf(poly, t, 0.254829592f);
   poly *= t;
-  const float y = 1.0f - poly * __expf(-ax * ax);
+  // exp(-x^2) = 2^(-x^2 log2 e)
+  const float y = 1.0f - poly * __builtin_amdgcn_exp2f(-1.4426950408889634f * ax * ax);
   return copysignf(y, x);
 }
 
@@ -57,11 +58,13 @@ __device__ __forceinline__ float gelu_erf(float x) {
   return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f));
 }
 // 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)) exactly, so the tanh form of GELU is
-// x * sigmoid(2u) with u = sqrt(2/pi) (x + 0.044715 x^3).
+// x * sigmoid(2u) with u = sqrt(2/pi) (x + 0.044715 x^3).  exp(-2u) is taken
+// as 2^(-2u log2 e); the reciprocal is the hardware one (1 ulp): for very
+// negative x it sees +inf and gives 0.
 __device__ __forceinline__ float gelu_tanh(float x) {
-  const float c2 = 1.5957691216057308f;  // 2 sqrt(2 / pi)
-  const float u2 = c2 * (x + 0.044715f * x * x * x);
-  return x / (1.0f + __expf(-u2));
+  const float c2l = 2.3022081983f;   // 2 sqrt(2 / pi) log2(e)
+  const float e = __builtin_amdgcn_exp2f(-c2l * fmaf(0.044715f * x, x * x, x));
+  return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 // Apply the chain to v.  col: column (BIAS_COL); ch: channel (BIAS_CH);

@@ -98,7 +98,7 @@ static GemmScratch gemm_scratch(const Plan& p, const Subkernel& sk, int impl) {
   const GemmSpec& g = sk.gemm;
   GemmScratch s{};
   s.mfma = use_mfma(p, sk, impl);
-  const int64_t tn = s.mfma ? kMfmaTileN : 64;
+  const int64_t tn = s.mfma ? kGemmTileN : 64;
   s.n_tiles = (g.N + tn - 1) / tn;
   if (g.ln) s.ln_bytes = align256(s.mfma ? g.M * g.K * elem_size(p.dtype) : 2 * g.M * 4);
   if (s.mfma && g.layout == 1) s.bt_bytes = align256(g.batch * g.heads * g.N * g.K * 2);
@@ -194,7 +194,7 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
   const int dt = p.dtype;
   switch (sk.family) {
     case MK_FAM_EW:
-      return hip_check(timed([&] { return launch_ew(dt, ew_args(sk.ew, vals, out, impl), st); }),
+      return hip_check(timed([&] { return launch_ew(dt, ew_args(sk.ew, vals, out, impl), st, impl); }),
                        "element-wise");
     case MK_FAM_ROW: {
       const RowSpec& r = sk.row;

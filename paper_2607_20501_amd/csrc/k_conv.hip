@@ -79,7 +79,7 @@ __global__ void gap_finish_kernel(const float* partial, int64_t N, int64_t K, in
 
 bool conv_mfma_supported(int dtype, const ConvArgs& a) {
   if (dtype != MK_BF16 || a.C % 32 || (a.P * a.Q) % 8) return false;
-  if (a.gap && a.P * a.Q < kMfmaTileN) return false;   // a tile spans at most two images
+  if (a.gap && a.P * a.Q < kConvTileN) return false;   // a tile spans at most two images
   const int64_t xp = a.N * (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C * 2;
   return xp < ((int64_t)1 << 31) && a.K * a.R * a.S * a.C * 2 < ((int64_t)1 << 31);
 }
@@ -89,7 +89,7 @@ ConvScratch conv_mfma_scratch(const ConvArgs& a) {
   auto al = [](int64_t b) { return (b + 255) / 256 * 256; };
   s.xp_bytes = al(a.N * (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C * 2);
   s.wp_bytes = al(a.K * a.R * a.S * a.C * 2);
-  const int64_t tiles = (a.N * a.P * a.Q + kMfmaTileN - 1) / kMfmaTileN;
+  const int64_t tiles = (a.N * a.P * a.Q + kConvTileN - 1) / kConvTileN;
   s.partial_bytes = a.gap ? al(tiles * 2 * a.K * 4) : 0;
   return s;
 }
@@ -127,7 +127,7 @@ GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float
   g.epi = a.epi;
   g.terminal = a.gap ? TERM_GAP : TERM_NONE;
   g.partial = partial;
-  g.n_tiles = (g.N + kMfmaTileN - 1) / kMfmaTileN;
+  g.n_tiles = (g.N + kConvTileN - 1) / kConvTileN;
   g.conv = 1;
   g.cv_C = a.C;
   g.cv_Hp = a.H + 2 * a.pad;
@@ -142,7 +142,7 @@ GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float
 hipError_t launch_gap_finish(const ConvArgs& a, const float* partial, hipStream_t st) {
   const int64_t total = a.N * a.K;
   hipLaunchKernelGGL(gap_finish_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
-                     partial, a.N, a.K, a.P * a.Q, kMfmaTileN, (bf16*)a.y);
+                     partial, a.N, a.K, a.P * a.Q, kConvTileN, (bf16*)a.y);
   return hipGetLastError();
 }
 

@@ -1,0 +1,130 @@
+// Tuned element-wise subkernel (HBM-bound).  Each thread keeps four 16-byte
+// groups of 8 values in flight, applies the whole chain to a group at once
+// (one uniform branch per chain step, 16-byte loads of bias and residual
+// operands), and derives only the indices the chain reads -- column, row of a
+// score matrix, channel -- by 32-bit multiply-shift division.  Groups that do
+// not meet the vector conditions run on the simple kernels.
+#include "dev.hpp"
+#include "fastdiv.hpp"
+
+namespace mk {
+
+namespace {
+
+enum : uint32_t { NEED_COL = 1, NEED_ROW = 2, NEED_CH = 4 };
+
+struct EwFastArgs {
+  const void* x;
+  void* y;
+  uint32_t groups;   // numel / 8
+  uint32_t tail;     // numel % 8
+  uint32_t need;
+  FastDiv last, S, HW, C;
+  EwArgs full;       // 64-bit view for the ragged tail
+};
+
+constexpr int kIn = 4;   // groups in flight per thread
+
+template <typename T>
+__global__ __launch_bounds__(256) void ew_fast_kernel(EwFastArgs a) {
+  const T* x = (const T*)a.x;
+  T* y = (T*)a.y;
+  const uint32_t stride = gridDim.x * 256u * kIn;
+  for (uint32_t g0 = blockIdx.x * 256u * kIn + threadIdx.x; g0 < a.groups; g0 += stride) {
+    float v[kIn][8];
+#pragma unroll
+    for (int j = 0; j < kIn; ++j) {
+      const uint32_t g = g0 + j * 256u;
+      if (g < a.groups) ld8<T>(x + (int64_t)g * 8, true, 8, v[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < kIn; ++j) {
+      const uint32_t g = g0 + j * 256u;
+      if (g >= a.groups) continue;
+      const uint32_t i0 = g * 8;
+      uint32_t col = 0, row = 0, ch = 0;
+      if (a.need & NEED_COL) col = a.last.mod(i0);
+      if (a.need & NEED_ROW) row = a.S.mod(a.S.div(i0));
+      if (a.need & NEED_CH) ch = a.C.mod(a.HW.div(i0));
+      epi_apply8<T>(a.full.epi, v[j], row, col, ch, 8, i0, true);
+      if constexpr (sizeof(T) == 2) {
+        uint4 o;
+        o.x = (uint32_t)f2bf(v[j][0]) | ((uint32_t)f2bf(v[j][1]) << 16);
+        o.y = (uint32_t)f2bf(v[j][2]) | ((uint32_t)f2bf(v[j][3]) << 16);
+        o.z = (uint32_t)f2bf(v[j][4]) | ((uint32_t)f2bf(v[j][5]) << 16);
+        o.w = (uint32_t)f2bf(v[j][6]) | ((uint32_t)f2bf(v[j][7]) << 16);
+        *(uint4*)(y + (int64_t)i0) = o;
+      } else {
+        *(float4*)(y + (int64_t)i0) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+        *(float4*)(y + (int64_t)i0 + 4) = make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
+      }
+    }
+  }
+  // the last numel % 8 elements, one per thread of block 0
+  if (blockIdx.x == 0 && threadIdx.x < a.tail) {
+    const EwArgs& f = a.full;
+    const int64_t i = (int64_t)a.groups * 8 + threadIdx.x;
+    float t = ld<T>(x, i);
+    t = epi_apply<T>(f.epi, t, (i / f.S) % f.S, i % f.last, (i / f.HW) % f.C, i);
+    st<T>(y, i, t);
+  }
+}
+
+bool aligned16(const void* p) { return (uintptr_t)p % 16 == 0; }
+
+}  // namespace
+
+bool ew_fast_supported(const EwArgs& a) {
+  if (a.numel < 1 || a.numel > (int64_t)0xFFFFFFF0) return false;
+  if (!aligned16(a.x) || !aligned16(a.y)) return false;
+  if (a.last < 1 || a.S < 1 || a.HW < 1 || a.C < 1) return false;
+  for (int i = 0; i < a.epi.n; ++i) {
+    switch (a.epi.code[i]) {
+      case EPI_BIAS_COL:
+        if (a.last % 8 || !aligned16(a.epi.ptr[i])) return false;
+        break;
+      case EPI_ADD:
+        if (!aligned16(a.epi.ptr[i])) return false;
+        break;
+      case EPI_BIAS_CH:
+        if (a.HW % 8) return false;
+        break;
+      case EPI_CAUSAL:
+      case EPI_CAUSAL_STRICT:
+        if (a.last % 8 || a.S % 8) return false;
+        break;
+      default:
+        break;
+    }
+  }
+  return a.last <= 0xFFFFFFFFll && a.S <= 0xFFFFFFFFll && a.HW <= 0xFFFFFFFFll &&
+         a.C <= 0xFFFFFFFFll;
+}
+
+hipError_t launch_ew_fast(int dtype, const EwArgs& a, hipStream_t st) {
+  EwFastArgs f{};
+  f.x = a.x;
+  f.y = a.y;
+  f.groups = (uint32_t)(a.numel / 8);
+  f.tail = (uint32_t)(a.numel % 8);
+  for (int i = 0; i < a.epi.n; ++i) {
+    const int c = a.epi.code[i];
+    if (c == EPI_BIAS_COL) f.need |= NEED_COL;
+    if (c == EPI_CAUSAL || c == EPI_CAUSAL_STRICT) f.need |= NEED_COL | NEED_ROW;
+    if (c == EPI_BIAS_CH) f.need |= NEED_CH;
+  }
+  f.last = FastDiv((uint32_t)a.last);
+  f.S = FastDiv((uint32_t)a.S);
+  f.HW = FastDiv((uint32_t)a.HW);
+  f.C = FastDiv((uint32_t)a.C);
+  f.full = a;
+  int64_t blocks = ((int64_t)f.groups + 256 * kIn - 1) / (256 * kIn);
+  blocks = std::max<int64_t>(1, std::min<int64_t>(blocks, 65536));
+  if (dtype == MK_BF16)
+    hipLaunchKernelGGL(ew_fast_kernel<bf16>, dim3((unsigned)blocks), dim3(256), 0, st, f);
+  else
+    hipLaunchKernelGGL(ew_fast_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, f);
+  return hipGetLastError();
+}
+
+}  // namespace mk

@@ -11,13 +11,18 @@
 // (App. I.1: "may need split at softmax due to reduction").
 //
 // Design for CDNA4:
-//  * 256 x 256 output tile per workgroup, K in 32-deep slices; 4 waves in a
-//    2 x 2 arrangement, each owning 128 x 128 = 4 x 4 tiles of
-//    v_mfma_f32_32x32x16_bf16 (256 fp32 accumulators per lane).
-//  * Operands move HBM -> LDS with buffer_load ... lds (no register staging):
-//    a 4-stage ring of 32 KB slices keeps three slices in flight while the
-//    MFMAs consume the fourth; one barrier per slice.  Out-of-range lanes read
-//    zeros through the buffer descriptor's range check (ragged M / N / K).
+//  * Plain GEMMs: a 256 x 256 output tile per workgroup, K in 32-deep
+//    slices, eight waves (two per SIMD) in a 2 x 4 arrangement, each owning
+//    128 x 64 = 4 x 2 tiles of v_mfma_f32_32x32x16_bf16 (128 fp32
+//    accumulators per lane).  Conv GEMMs: 256 x 128 tiles, four waves, two
+//    workgroups per CU.
+//  * Operands move HBM -> LDS with buffer_load ... lds (no register staging)
+//    into a ring of 32 KB slices (4 stages; 3 for conv) with one barrier per
+//    slice.  Out-of-range lanes read zeros through the buffer descriptor's
+//    range check (ragged M / N / K).
+//  * Plain GEMMs read MFMA fragments one 16-deep half-slice ahead of the
+//    MFMAs that use them, with the barrier between the two halves, so the
+//    matrix cores are fed across the barrier.
 //  * LDS rows are 64 bytes (four 16-byte chunks); chunk c of row r sits at
 //    chunk c ^ (((r >> 1) ^ (r >> 3)) & 3), so the lanes served together by a
 //    128-bit fragment read hit distinct banks.  Each lane's global address is
@@ -30,6 +35,7 @@
 //  * The epilogue stages 32-row slabs of accumulators through LDS so each
 //    lane finishes 8 consecutive columns and writes them with one 16-byte
 //    store.
+
 #include "dev.hpp"
 
 namespace mk {
@@ -39,10 +45,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 32;
-constexpr int kStages = 4;
-constexpr int kTileBytes = BM * BK * 2;           // 16 KB per operand slice
-constexpr int kStageBytes = 2 * kTileBytes;       // 32 KB per stage
+constexpr int BM = 256, BK = 32;
+constexpr int kTileBytes = BM * BK * 2;           // 16 KB A slice
 constexpr int kGroupM = 8;                        // tile rows per locality group
 constexpr int kXcds = 8;
 
@@ -88,12 +92,13 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff, 
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Direct HBM -> LDS loads of one operand slice (1024 16-byte chunks).  For
+// Direct HBM -> LDS loads of one operand slice (ROWS x 32 bf16 = ROWS*4
+// 16-byte chunks).  For
 // load q of wave w, lane i fills LDS chunk p = (q*WAVES + w)*64 + i, i.e. row
 // p/4, physical chunk p%4, whose logical chunk is (p%4) ^ swz(row).
-template <int WAVES>
+template <int WAVES, int ROWS>
 struct SliceLoader {
-  static constexpr int LQ = 16 / WAVES;   // loads per thread per operand slice
+  static constexpr int LQ = ROWS * 4 / (64 * WAVES);   // loads per thread per slice
   __amdgpu_buffer_rsrc_t src;
   uint32_t voff[LQ];   // byte offset at k0 = 0, kOob if the row is out of range
   int lchunk[LQ];      // logical 16-byte chunk of this lane's loads
@@ -158,7 +163,7 @@ template <int NJ>
 __device__ __forceinline__ void load_frags(const char* stage, int kk, int rowbase, int colbase,
                                            int lr, int lh, Frags<NJ>& f) {
   const char* la = stage;
-  const char* lb = stage + kTileBytes;
+  const char* lb = stage + kTileBytes;   // B slice follows the 256-row A slice
 #pragma unroll
   for (int i = 0; i < 4; ++i)
     f.a[i] = *(const bf16x8*)(la + lds_off(rowbase + i * 32 + lr, kk * 2 + lh));
@@ -205,9 +210,15 @@ __device__ __forceinline__ uint32_t conv_koff(const GemmArgs& a, int64_t k0) {
   return (uint32_t)(((r * a.cv_Wp + s) * a.cv_C + c0) * 2);
 }
 
-template <int WN, int CONV>
-__global__ __launch_bounds__(128 * WN, 1) void gemm_bf16_mfma_kernel(GemmArgs a) {
+// Variants: WN waves along N (2 rows of waves), BN columns per tile, STG
+// ring stages.  <4, 256, 4>: eight waves share one 256 x 256 tile (one
+// workgroup per CU).  <2, 128, 3>: four waves on a 256 x 128 tile in 72 KB of
+// LDS, so two independent workgroups share each CU.
+template <int WN, int BN, int STG, int CONV, int PIPE>
+__global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_kernel(GemmArgs a) {
   constexpr int WAVES = 2 * WN, THREADS = 64 * WAVES;
+  constexpr int kStages = STG;
+  constexpr int kStageBytes = (BM + BN) * BK * 2;
   constexpr int WTN = BN / WN;        // wave tile columns
   constexpr int NJ = WTN / 32;        // 32-wide column tiles per wave
   constexpr int LD = WTN + 8;         // epilogue slab row stride (floats)
@@ -235,7 +246,8 @@ __global__ __launch_bounds__(128 * WN, 1) void gemm_bf16_mfma_kernel(GemmArgs a)
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = (int)((a.K + BK - 1) / BK);
-  SliceLoader<WAVES> la, lb;
+  SliceLoader<WAVES, BM> la;
+  SliceLoader<WAVES, BN> lb;
   la.init(A, a.M, a.lda, m0);
   const int64_t PQ = a.cv_P * a.cv_Q;
   if (CONV) {
@@ -261,37 +273,80 @@ __global__ __launch_bounds__(128 * WN, 1) void gemm_bf16_mfma_kernel(GemmArgs a)
       issue_b(smem + s * kStageBytes + kTileBytes, (int64_t)s * BK);
     }
 
-  constexpr int LPS = 2 * (16 / WAVES);   // loads per thread per slice
-  for (int kt = 0; kt < nk; ++kt) {
-    // Slice kt has landed once at most the loads of the (up to two) later
-    // slices are outstanding.
-    const int later = min(kStages - 2, nk - 1 - kt);
-    if (later >= 2)
+  constexpr int LPS = SliceLoader<WAVES, BM>::LQ + SliceLoader<WAVES, BN>::LQ;
+  // Wait until at most `later` slices issued after the one needed are still
+  // in flight (each slice is LPS loads of this wave, issued in order).
+  auto wait_slices = [](int later) {
+    if (later >= 3)
+      wait_vm<3 * LPS>();
+    else if (later == 2)
       wait_vm<2 * LPS>();
     else if (later == 1)
       wait_vm<LPS>();
     else
       wait_vm<0>();
-    // A bare barrier: __syncthreads() would also drain every outstanding load
-    // (its fence), which defeats the ring.  The slice's own loads are complete
-    // (vmcnt above), and fragment reads of the slot about to be refilled were
-    // consumed by MFMAs before this point.
+  };
+  if (PIPE) {
+    // Fragment reads run one half-step (k16) ahead of the MFMAs, so the
+    // barrier sits between the two halves of a slice: the MFMAs of half 0 of
+    // slice kt overlap the reads of its half 1, those of half 1 the reads of
+    // half 0 of slice kt+1.  At the barrier of step kt every wave has
+    // consumed slice kt-1 (its half-1 MFMAs waited on those reads), so that
+    // slot takes slice kt+STG-1.
+    wait_slices(min(kStages - 2, nk - 1));
     __builtin_amdgcn_s_barrier();
-    const int nxt = kt + kStages - 1;
-    if (nxt < nk) {
-      char* st = smem + (nxt % kStages) * kStageBytes;
-      la.issue(st, (int64_t)nxt * BK, a.K);
-      issue_b(st + kTileBytes, (int64_t)nxt * BK);
-    }
-    const char* cur = smem + (kt % kStages) * kStageBytes;
     Frags<NJ> f0, f1;
-    load_frags<NJ>(cur, 0, rowbase, colbase, lr, lh, f0);
-    load_frags<NJ>(cur, 1, rowbase, colbase, lr, lh, f1);
+    load_frags<NJ>(smem, 0, rowbase, colbase, lr, lh, f0);
+    // (The last step is peeled so the loop body has no branch between the
+    // two groups of reads, which lets each MFMA group wait only for its own.)
+    for (int kt = 0; kt < nk - 1; ++kt) {
+      load_frags<NJ>(smem + (kt % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step<NJ>(f0, acc);
+      __builtin_amdgcn_sched_barrier(0);
+      wait_slices(min(kStages - 3, nk - 2 - kt));
+      __builtin_amdgcn_s_barrier();
+      const int nxt = kt + kStages - 1;
+      if (nxt < nk) {
+        char* st = smem + (nxt % kStages) * kStageBytes;
+        la.issue(st, (int64_t)nxt * BK, a.K);
+        issue_b(st + kTileBytes, (int64_t)nxt * BK);
+      }
+      load_frags<NJ>(smem + ((kt + 1) % kStages) * kStageBytes, 0, rowbase, colbase, lr, lh, f0);
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step<NJ>(f1, acc);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    load_frags<NJ>(smem + ((nk - 1) % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
     __builtin_amdgcn_sched_barrier(0);
     mfma_step<NJ>(f0, acc);
-    __builtin_amdgcn_sched_barrier(0);
     mfma_step<NJ>(f1, acc);
-    __builtin_amdgcn_sched_barrier(0);
+  } else {
+    for (int kt = 0; kt < nk; ++kt) {
+      // Slice kt has landed once at most the loads of the later slices are
+      // outstanding.
+      wait_slices(min(kStages - 2, nk - 1 - kt));
+      // A bare barrier: __syncthreads() would also drain every outstanding
+      // load (its fence), which defeats the ring.  The slice's own loads are
+      // complete (vmcnt above), and fragment reads of the slot about to be
+      // refilled were consumed by MFMAs before this point.
+      __builtin_amdgcn_s_barrier();
+      const int nxt = kt + kStages - 1;
+      if (nxt < nk) {
+        char* st = smem + (nxt % kStages) * kStageBytes;
+        la.issue(st, (int64_t)nxt * BK, a.K);
+        issue_b(st + kTileBytes, (int64_t)nxt * BK);
+      }
+      const char* cur = smem + (kt % kStages) * kStageBytes;
+      Frags<NJ> f0, f1;
+      load_frags<NJ>(cur, 0, rowbase, colbase, lr, lh, f0);
+      load_frags<NJ>(cur, 1, rowbase, colbase, lr, lh, f1);
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step<NJ>(f0, acc);
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step<NJ>(f1, acc);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 
   // ---------------------------------------------------------------- epilogue
@@ -518,7 +573,7 @@ bool gemm_mfma_supported(int dtype, const GemmArgs& a) {
   // Buffer-resource ranges are 32-bit: every operand slice must stay below 2 GB.
   const int64_t lim = (int64_t)1 << 31;
   if (a.M * a.lda * 2 >= lim || a.N * (a.layout == 0 ? a.ldb : a.K) * 2 >= lim) return false;
-  const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + 127) / 128);
   return tiles < (1ll << 31) && a.batch * a.heads <= 65535;
 }
 
@@ -552,13 +607,18 @@ hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
     return hipErrorInvalidValue;
   }
   if (((uintptr_t)a.A | (uintptr_t)a.B) % 16) return hipErrorInvalidValue;
-  const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  // Plain GEMMs: 256 x 256 tiles, 8 waves, 4-stage ring.  Conv GEMMs: 256 x 128
+  // tiles, 4 waves, 3 stages -- the gathered B rows make the wider tile's
+  // address set-up cost more than its extra reuse saves.
+  const int64_t bn = a.conv ? kConvTileN : kGemmTileN;
+  const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + bn - 1) / bn);
   dim3 grid((unsigned)tiles, (unsigned)(a.batch * a.heads));
-  // Eight waves (two per SIMD) measured faster than four on every workload.
+  // (The conv variant keeps the plain loop: with three stages the pipelined
+  // one would leave only one step of load latency hiding.)
   if (a.conv)
-    hipLaunchKernelGGL((gemm_bf16_mfma_kernel<4, 1>), grid, dim3(512), 0, st, a);
+    hipLaunchKernelGGL((gemm_bf16_mfma_kernel<2, kConvTileN, 3, 1, 0>), grid, dim3(256), 0, st, a);
   else
-    hipLaunchKernelGGL((gemm_bf16_mfma_kernel<4, 0>), grid, dim3(512), 0, st, a);
+    hipLaunchKernelGGL((gemm_bf16_mfma_kernel<4, kGemmTileN, 4, 0, 1>), grid, dim3(512), 0, st, a);
   return hipGetLastError();
 }
 

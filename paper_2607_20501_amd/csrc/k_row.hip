@@ -1,0 +1,154 @@
+// Tuned row kernels (HBM-bound, no element-wise prologue): one wave per row, the row held in registers
+// after one pass of 16-byte loads, reductions by wave shuffles.  Row-sum,
+// global average pool, softmax (max subtracted, App. D), LayerNorm (mean, then
+// the biased variance of the centred values; App. H.2 / App. I.2).  Each value
+// is read from HBM once and each output written once.
+#include "dev.hpp"
+
+namespace mk {
+
+namespace {
+
+template <typename T>
+constexpr int kEpv = 16 / sizeof(T);   // elements per 16-byte vector
+
+template <typename T>
+__device__ __forceinline__ void ld_vec(const T* p, float* out) {
+  float t[8];
+  ld8<T>(p, true, 8, t);
+#pragma unroll
+  for (int k = 0; k < kEpv<T>; ++k) out[k] = t[k];
+}
+
+template <typename T>
+__device__ __forceinline__ void st_vec(T* p, const float* v) {
+  if constexpr (sizeof(T) == 2) {
+    uint4 o;
+    o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+    o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+    o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
+    o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+    *(uint4*)p = o;
+  } else {
+    *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+  }
+}
+
+// NV 16-byte vectors per lane cover the row (L <= 64 * NV * kEpv, L a
+// multiple of kEpv); lane l owns vectors l, l + 64, ...
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void row_wave_kernel(RowArgs a) {
+  constexpr int E = kEpv<T>;
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= a.rows) return;   // whole wave exits together
+  const int64_t L = a.len;
+  const T* x = (const T*)a.x + r * L;
+  float v[NV][E];
+  bool ok[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int64_t c = (int64_t)(i * 64 + lane) * E;
+    ok[i] = c < L;
+    if (ok[i]) ld_vec<T>(x + c, v[i]);
+  }
+  if (a.op == MK_OP_ROWSUM || a.op == MK_OP_GAP) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (ok[i])
+#pragma unroll
+        for (int k = 0; k < E; ++k) s += v[i][k];
+    s = warp_sum(s);
+    if (lane == 0) st<T>((T*)a.y, r, a.op == MK_OP_GAP ? s / (float)L : s);
+    return;
+  }
+  T* y = (T*)a.y + r * L;
+  if (a.op == MK_OP_SOFTMAX) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (ok[i])
+#pragma unroll
+        for (int k = 0; k < E; ++k) m = fmaxf(m, v[i][k]);
+    m = warp_max(m);
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (ok[i])
+#pragma unroll
+        for (int k = 0; k < E; ++k) {
+          v[i][k] = __expf(v[i][k] - m);
+          s += v[i][k];
+        }
+    const float inv = 1.0f / warp_sum(s);
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (ok[i]) {
+#pragma unroll
+        for (int k = 0; k < E; ++k) v[i][k] *= inv;
+        st_vec<T>(y + (int64_t)(i * 64 + lane) * E, v[i]);
+      }
+    return;
+  }
+  // LayerNorm
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    if (ok[i])
+#pragma unroll
+      for (int k = 0; k < E; ++k) s += v[i][k];
+  const float mu = warp_sum(s) / (float)L;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    if (ok[i])
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        const float d = v[i][k] - mu;
+        q += d * d;
+      }
+  const float rstd = rsqrtf(warp_sum(q) / (float)L + a.eps);
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    if (ok[i]) {
+      const int64_t c = (int64_t)(i * 64 + lane) * E;
+      float g[E], b[E];
+      ld_vec<T>((const T*)a.gamma + c, g);
+      ld_vec<T>((const T*)a.beta + c, b);
+#pragma unroll
+      for (int k = 0; k < E; ++k) v[i][k] = (v[i][k] - mu) * rstd * g[k] + b[k];
+      st_vec<T>(y + c, v[i]);
+    }
+}
+
+template <typename T>
+hipError_t launch_row_wave_t(const RowArgs& a, hipStream_t st) {
+  constexpr int E = kEpv<T>;
+  const int64_t nv = (a.len + 64 * E - 1) / (64 * E);
+  const dim3 grid((unsigned)((a.rows + 3) / 4)), block(256);
+  switch (nv) {
+    case 1: hipLaunchKernelGGL((row_wave_kernel<T, 1>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((row_wave_kernel<T, 2>), grid, block, 0, st, a); break;
+    case 3: case 4: hipLaunchKernelGGL((row_wave_kernel<T, 4>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((row_wave_kernel<T, 8>), grid, block, 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool row_wave_supported(int dtype, const RowArgs& a) {
+  const int E = dtype == MK_BF16 ? 8 : 4;
+  // (Groups with an element-wise prologue run on the simple row kernel.)
+  if (a.pre.epi.n || a.len % E || a.len > 64 * 8 * E || a.rows < 1) return false;
+  if (((uintptr_t)a.x | (uintptr_t)a.y) % 16) return false;
+  if (a.op == MK_OP_LAYERNORM && ((uintptr_t)a.gamma | (uintptr_t)a.beta) % 16) return false;
+  return a.rows / 4 < (1ll << 31);
+}
+
+hipError_t launch_row_wave(int dtype, const RowArgs& a, hipStream_t st) {
+  return dtype == MK_BF16 ? launch_row_wave_t<bf16>(a, st) : launch_row_wave_t<float>(a, st);
+}
+
+}  // namespace mk

@@ -18,55 +18,67 @@ __global__ void ew_simple_kernel(EwArgs a) {
   }
 }
 
-// Vectorised form: each thread owns 8 consecutive elements (one 16-byte bf16
-// or two 16-byte fp32 accesses); index arithmetic is done once per group.
+// Vectorised form: a thread owns groups of 8 consecutive elements (one
+// 16-byte bf16 or two 16-byte fp32 accesses) and keeps 4 groups in flight;
+// index arithmetic is done once per group.
+template <typename T>
+__device__ __forceinline__ void ew_load8(const T* x, int64_t i0, float (&v)[8]) {
+  ld8<T>(x + i0, true, 8, v);
+}
+
+template <typename T>
+__device__ __forceinline__ void ew_store8(T* y, int64_t i0, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    uint4 raw;
+    raw.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+    raw.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+    raw.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
+    raw.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+    *(uint4*)(y + i0) = raw;
+  } else {
+    *(float4*)(y + i0) = make_float4(v[0], v[1], v[2], v[3]);
+    *(float4*)(y + i0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void ew_chain8(const EwArgs& a, int64_t i0, float (&v)[8]) {
+  int64_t col = i0 % a.last, row = (i0 / a.S) % a.S, ch = (i0 / a.HW) % a.C;
+  int64_t inrow = i0 % a.HW;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    v[k] = epi_apply<T>(a.epi, v[k], row, col, ch, i0 + k);
+    if (++col == a.last) {
+      col = 0;
+      if (++row == a.S) row = 0;
+    }
+    if (++inrow == a.HW) {
+      inrow = 0;
+      if (++ch == a.C) ch = 0;
+    }
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void ew_vec_kernel(EwArgs a) {
+  constexpr int kIn = 4;   // groups in flight per thread
   const int64_t groups = a.numel / 8;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < groups; g += stride) {
-    const int64_t i0 = g * 8;
-    float v[8];
-    if constexpr (sizeof(T) == 2) {
-      uint4 raw = *(const uint4*)((const T*)a.x + i0);
-      const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+  const int64_t span = (int64_t)gridDim.x * blockDim.x * kIn;
+  for (int64_t g0 = (int64_t)blockIdx.x * blockDim.x * kIn + threadIdx.x; g0 < groups;
+       g0 += span) {
+    float v[kIn][8];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        v[2 * k] = __uint_as_float(w[k] << 16);
-        v[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
-      }
-    } else {
-      float4 r0 = *(const float4*)((const float*)a.x + i0);
-      float4 r1 = *(const float4*)((const float*)a.x + i0 + 4);
-      v[0] = r0.x; v[1] = r0.y; v[2] = r0.z; v[3] = r0.w;
-      v[4] = r1.x; v[5] = r1.y; v[6] = r1.z; v[7] = r1.w;
+    for (int j = 0; j < kIn; ++j) {
+      const int64_t g = g0 + (int64_t)j * blockDim.x;
+      if (g < groups) ew_load8<T>((const T*)a.x, g * 8, v[j]);
     }
-    if (a.epi.n) {
-      int64_t col = i0 % a.last, row = (i0 / a.S) % a.S, ch = (i0 / a.HW) % a.C;
-      int64_t inrow = i0 % a.HW;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        v[k] = epi_apply<T>(a.epi, v[k], row, col, ch, i0 + k);
-        if (++col == a.last) {
-          col = 0;
-          if (++row == a.S) row = 0;
-        }
-        if (++inrow == a.HW) {
-          inrow = 0;
-          if (++ch == a.C) ch = 0;
-        }
+    for (int j = 0; j < kIn; ++j) {
+      const int64_t g = g0 + (int64_t)j * blockDim.x;
+      if (g < groups) {
+        if (a.epi.n) ew_chain8<T>(a, g * 8, v[j]);
+        ew_store8<T>((T*)a.y, g * 8, v[j]);
       }
-    }
-    if constexpr (sizeof(T) == 2) {
-      uint4 raw;
-      raw.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-      raw.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-      raw.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
-      raw.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
-      *(uint4*)((T*)a.y + i0) = raw;
-    } else {
-      *(float4*)((float*)a.y + i0) = make_float4(v[0], v[1], v[2], v[3]);
-      *(float4*)((float*)a.y + i0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
     }
   }
   // ragged tail
@@ -86,11 +98,12 @@ static int grid_for(int64_t work, int per_block) {
   return (int)(g < 1 ? 1 : g);
 }
 
-hipError_t launch_ew(int dtype, const EwArgs& a, hipStream_t st) {
+hipError_t launch_ew(int dtype, const EwArgs& a, hipStream_t st, int impl) {
   if (a.numel == 0) return hipSuccess;
+  if (impl != MK_IMPL_SIMPLE && ew_fast_supported(a)) return launch_ew_fast(dtype, a, st);
   const bool aligned = ((uintptr_t)a.x % 16 == 0) && ((uintptr_t)a.y % 16 == 0);
   if (aligned) {
-    const int g = grid_for(a.numel / 8 + 1, 256);
+    const int g = grid_for(a.numel / 32 + 1, 256);
     if (dtype == 1)
       hipLaunchKernelGGL(ew_vec_kernel<bf16>, dim3(g), dim3(256), 0, st, a);
     else
@@ -166,8 +179,9 @@ __global__ __launch_bounds__(256) void row_kernel(RowArgs a) {
   }
 }
 
-hipError_t launch_row(int dtype, const RowArgs& a, hipStream_t st, int /*impl*/) {
+hipError_t launch_row(int dtype, const RowArgs& a, hipStream_t st, int impl) {
   if (a.rows == 0) return hipSuccess;
+  if (impl != MK_IMPL_SIMPLE && row_wave_supported(dtype, a)) return launch_row_wave(dtype, a, st);
   if (dtype == 1)
     hipLaunchKernelGGL(row_kernel<bf16>, dim3((unsigned)a.rows), dim3(256), 0, st, a);
   else

@@ -80,8 +80,12 @@ struct AttnArgs {
 };
 
 // dtype: 0 float32, 1 bfloat16 (mk_dtype).
-hipError_t launch_ew(int dtype, const EwArgs& a, hipStream_t st);
+hipError_t launch_ew(int dtype, const EwArgs& a, hipStream_t st, int impl);
 hipError_t launch_row(int dtype, const RowArgs& a, hipStream_t st, int impl);
+// Tuned row kernel: one wave per row, the row in registers (len a multiple of
+// 8 bf16 / 4 fp32 elements, at most 4096 / 2048, 16-byte aligned buffers).
+bool row_wave_supported(int dtype, const RowArgs& a);
+hipError_t launch_row_wave(int dtype, const RowArgs& a, hipStream_t st);
 hipError_t launch_ln_stats(int dtype, const void* x, int64_t rows, int64_t len, float eps,
                            float* stats, hipStream_t st);
 hipError_t launch_gemm_simple(int dtype, const GemmArgs& a, hipStream_t st);
@@ -93,7 +97,14 @@ hipError_t launch_conv_simple(int dtype, const ConvArgs& a, hipStream_t st);
 hipError_t launch_attn_simple(int dtype, const AttnArgs& a, hipStream_t st);
 
 // Tuned kernels.
-constexpr int64_t kMfmaTileN = 256;   // column tile of the bf16 MFMA GEMM
+// Tuned element-wise kernel (k_ew.hip): 16-byte groups, 32-bit index
+// arithmetic; ew_fast_supported() states when it applies.
+bool ew_fast_supported(const EwArgs& a);
+hipError_t launch_ew_fast(int dtype, const EwArgs& a, hipStream_t st);
+// Column tiles of the bf16 MFMA GEMM for plain GEMMs and for conv GEMMs; the
+// per-tile partial layouts of the terminal finishers follow them.
+constexpr int kGemmTileN = 256;
+constexpr int kConvTileN = 128;
 bool gemm_mfma_supported(int dtype, const GemmArgs& a);
 // The MFMA kernel takes B as [N, K]; a [K, N] operand (layout 1) is first
 // transposed into scratch of gemm_mfma_bt_bytes() bytes, and gemm_with_bt()
