@@ -110,6 +110,23 @@ def time_module(mod, ins, out, ws, steps, warmup):
     return ms, per_launch
 
 
+def median_flushed(mod, ins, out, ws, runs, flush):
+    """Median time (ms) of `runs` individually timed runs, each preceded by a
+    write of the `flush` buffer so that no operand is served from L2 or the
+    256 MB Infinity Cache."""
+    import statistics
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(runs)]
+    for i, (a, b) in enumerate(ev):
+        flush.fill_(i & 0x7F)
+        a.record()
+        mod.run(ins, out, ws)
+        b.record()
+    torch.cuda.synchronize()
+    return statistics.median(a.elapsed_time(b) for a, b in ev)
+
+
 def cpu_baseline(module, host, rows, out_dev):
     """The oracle on the first `rows` rows of a row-independent module; also
     compares those rows of the GPU output."""
@@ -153,6 +170,9 @@ def main():
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
                     help="run one plain device copy of this size first (counter calibration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--protocol-runs", type=int, default=100,
+                    help="individually timed runs (1 GiB cache flush before each) for the "
+                         "median; 0 skips")
     ap.add_argument("--seed", type=int, default=0)
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -199,6 +219,23 @@ def main():
         # the split run overwrote nothing the fused output depends on; rerun fused
         fused.run(ins, out, ws)
         torch.cuda.synchronize()
+
+    if args.protocol_runs:
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        med = {"runs": args.protocol_runs, "flush_bytes": 1 << 30,
+               "fused_median_ms": median_flushed(fused, ins, out, ws, args.protocol_runs, flush)}
+        if split is not None:
+            out_s = mk.out_tensor(module, split.info["out_shape"])
+            med["split_median_ms"] = median_flushed(split, ins, out_s, ws, args.protocol_runs,
+                                                    flush)
+            med["fused_vs_split_speedup"] = med["split_median_ms"] / med["fused_median_ms"]
+            del out_s
+            fused.run(ins, out, ws)
+        med["fused_tflops"] = flops / (med["fused_median_ms"] * 1e-3) / 1e12
+        del flush
+        torch.cuda.synchronize()
+        result["median_protocol"] = med
+        log(f"median protocol: {med}")
 
     # dominant kernel of the timed composition
     names = launch_names(fused)
