@@ -132,6 +132,7 @@ typedef struct {
   int32_t impl;                   /* selected implementation id */
   int32_t n_launches;             /* kernel launches of the selected implementation */
   int64_t scratch_bytes;          /* scratch the selected implementation uses */
+  int32_t uses_mfma;              /* 1: the contraction runs on the matrix cores */
 } mk_subkernel_info_t;
 
 /* Fill group_of_op[n_ops] with a preset decomposition.  preset 0 = split (one

@@ -118,6 +118,23 @@ __device__ __forceinline__ void ld8(const T* p, bool vec, int valid, float (&out
   }
 }
 
+// Store 8 consecutive values to p[0..7] (16-byte aligned): one 16-byte store
+// of bf16, two of fp32.
+template <typename T>
+__device__ __forceinline__ void st8(T* p, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    uint4 o;
+    o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+    o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+    o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
+    o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+    *(uint4*)p = o;
+  } else {
+    *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+    *(float4*)(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
 // The chain applied to 8 consecutive columns col0.. of one row (flat0 is the
 // offset of column col0 in residual operands).  One uniform switch per step;
 // `vec` says that 16-byte operand accesses are aligned and in range.

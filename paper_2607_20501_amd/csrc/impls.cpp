@@ -101,7 +101,7 @@ static GemmScratch gemm_scratch(const Plan& p, const Subkernel& sk, int impl) {
   const int64_t tn = s.mfma ? kGemmTileN : 64;
   s.n_tiles = (g.N + tn - 1) / tn;
   if (g.ln) s.ln_bytes = align256(s.mfma ? g.M * g.K * elem_size(p.dtype) : 2 * g.M * 4);
-  if (s.mfma && g.layout == 1) s.bt_bytes = align256(g.batch * g.heads * g.N * g.K * 2);
+  if (s.mfma && g.layout == 1) s.bt_bytes = align256(g.batch * g.heads * g.N * g.K * elem_size(p.dtype));
   if (g.terminal == TERM_ROWSUM) s.partial_bytes = align256(g.M * s.n_tiles * 4);
   if (g.terminal == TERM_SOFTMAX) s.partial_bytes = align256(g.M * s.n_tiles * 8);
   return s;
@@ -123,7 +123,7 @@ static bool use_conv_mfma(const Plan& p, const Subkernel& sk, int impl) {
 int64_t impl_scratch(const Plan& p, const Subkernel& sk, int impl) {
   if (sk.family == MK_FAM_CONV) {
     if (!use_conv_mfma(p, sk, impl)) return 0;
-    const ConvScratch c = conv_mfma_scratch(conv_args(sk.conv));
+    const ConvScratch c = conv_mfma_scratch(p.dtype, conv_args(sk.conv));
     return c.xp_bytes + c.wp_bytes + c.partial_bytes;
   }
   if (sk.family != MK_FAM_GEMM) return 0;
@@ -133,6 +133,18 @@ int64_t impl_scratch(const Plan& p, const Subkernel& sk, int impl) {
 
 int64_t max_scratch_bytes(const Plan& p, const Subkernel& sk) {
   return std::max(impl_scratch(p, sk, MK_IMPL_TUNED), impl_scratch(p, sk, MK_IMPL_SIMPLE));
+}
+
+bool impl_uses_mfma(const Plan& p, const Subkernel& sk, int impl) {
+  if (sk.family == MK_FAM_GEMM) return use_mfma(p, sk, impl);
+  if (sk.family == MK_FAM_CONV) return use_conv_mfma(p, sk, impl);
+  if (sk.family == MK_FAM_ATTN && impl != MK_IMPL_SIMPLE) {
+    AttnArgs a{};
+    a.B = sk.attn.B; a.H = sk.attn.H; a.dh = sk.attn.dh; a.S = sk.attn.S;
+    a.causal = sk.attn.causal ? 1 : 0;
+    return attn_fused_supported(p.dtype, a);
+  }
+  return false;
 }
 
 int impl_launches(const Plan& p, const Subkernel& sk, int impl) {
@@ -264,7 +276,7 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       }
       if (gs.bt_bytes) {
         void* bt = sc;
-        mk_status s = hip_check(timed([&] { return launch_transpose_b(a, bt, st); }),
+        mk_status s = hip_check(timed([&] { return launch_transpose_b(dt, a, bt, st); }),
                                 "transpose B");
         if (s != MK_OK) return s;
         a = gemm_with_bt(a, bt);
@@ -302,18 +314,18 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
         return hip_check(timed([&] { return launch_conv_simple(dt, a, st); }), "conv");
       // Implicit GEMM: repack input and weights into scratch, run the MFMA
       // GEMM in conv mode, then (GAP) combine the per-tile partials.
-      const ConvScratch cs = conv_mfma_scratch(a);
+      const ConvScratch cs = conv_mfma_scratch(dt, a);
       char* xp = (char*)scratch;
       char* wp = xp + cs.xp_bytes;
       float* part = (float*)(wp + cs.wp_bytes);
-      mk_status s = hip_check(timed([&] { return launch_pack_nhwc(a, xp, st); }), "pack nhwc");
+      mk_status s = hip_check(timed([&] { return launch_pack_nhwc(dt, a, xp, st); }), "pack nhwc");
       if (s != MK_OK) return s;
-      s = hip_check(timed([&] { return launch_pack_krsc(a, wp, st); }), "pack krsc");
+      s = hip_check(timed([&] { return launch_pack_krsc(dt, a, wp, st); }), "pack krsc");
       if (s != MK_OK) return s;
       const GemmArgs g = conv_gemm_args(a, xp, wp, part);
       s = hip_check(timed([&] { return launch_gemm_mfma(dt, g, st); }), "conv gemm");
       if (s != MK_OK || !a.gap) return s;
-      return hip_check(timed([&] { return launch_gap_finish(a, part, st); }), "gap finish");
+      return hip_check(timed([&] { return launch_gap_finish(dt, a, part, st); }), "gap finish");
     }
     case MK_FAM_ATTN: {
       const AttnSpec& t = sk.attn;

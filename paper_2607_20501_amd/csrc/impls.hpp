@@ -16,6 +16,8 @@ int64_t impl_scratch(const Plan& p, const Subkernel& sk, int impl);
 // Largest scratch over the implementations of sk (so a swap never needs a
 // bigger workspace).
 int64_t max_scratch_bytes(const Plan& p, const Subkernel& sk);
+// Whether the implementation runs its contraction on the matrix cores.
+bool impl_uses_mfma(const Plan& p, const Subkernel& sk, int impl);
 
 // Optional launch-level timing: brackets each kernel launch with a pair of
 // HIP events taken from a pre-created pool (no synchronisation).

@@ -16,13 +16,55 @@ namespace mk {
 
 namespace {
 
-// x [N][C][H][W] -> xp [N][H+2pad][W+2pad][C], zero border.  One workgroup per
-// (64 padded positions, 64 channels, image); the tile is transposed in LDS so
-// both the reads (along positions) and the 16-byte writes (along channels)
-// are coalesced.
-__global__ __launch_bounds__(256) void pack_nhwc_kernel(const bf16* x, bf16* xp, int64_t C,
-                                                        int64_t H, int64_t W, int64_t pad) {
-  __shared__ bf16 tile[64][72];
+// x [N][C][H][W] -> xp [N][H+2pad][W+2pad][C], zero border.
+//
+// Row form (W <= 64, rows of whole 16-byte chunks): one workgroup per (padded
+// row hp, 64 channels, image).  Each (c, h) input row is one contiguous run
+// of W values, read in 16-byte chunks; the tile is transposed in LDS and the
+// padded row written as 16-byte channel chunks, border positions as zeros.
+template <typename T>
+__global__ __launch_bounds__(256) void pack_nhwc_rows_kernel(const T* x, T* xp, int64_t C,
+                                                             int64_t H, int64_t W, int64_t pad) {
+  constexpr int E = 16 / (int)sizeof(T);
+  __shared__ __attribute__((aligned(16))) T tile[64][64 + E];   // [w][channel]
+  const int64_t Hp = H + 2 * pad, Wp = W + 2 * pad;
+  const int64_t hp = blockIdx.x, c0 = (int64_t)blockIdx.y * 64, n = blockIdx.z;
+  const int64_t h = hp - pad;
+  const bool inside = h >= 0 && h < H;
+  const int t = threadIdx.x;
+  const int cpr = (int)(W / E);             // chunks per input row
+  if (inside) {
+    for (int idx = t; idx < 64 * cpr; idx += 256) {
+      const int cl = idx / cpr, j = idx % cpr;
+      const int64_t c = c0 + cl;
+      if (c >= C) continue;
+      const uint4 v = *(const uint4*)(x + ((n * C + c) * H + h) * W + j * E);
+      const T* e = (const T*)&v;
+#pragma unroll
+      for (int k = 0; k < E; ++k) tile[j * E + k][cl] = e[k];
+    }
+  }
+  __syncthreads();
+  constexpr int CPP = 64 / E;               // channel chunks per position
+  T* dst = xp + ((n * Hp + hp) * Wp) * C + c0;
+  for (int idx = t; idx < (int)Wp * CPP; idx += 256) {
+    const int64_t wp = idx / CPP;
+    const int cc = idx % CPP;
+    if (c0 + cc * E >= C) continue;
+    const int64_t w = wp - pad;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (inside && w >= 0 && w < W) v = *(const uint4*)&tile[w][cc * E];
+    *(uint4*)(dst + wp * C + cc * E) = v;
+  }
+}
+
+// General form: one workgroup per (64 padded positions, 64 channels, image),
+// one element per thread on the read side.
+template <typename T>
+__global__ __launch_bounds__(256) void pack_nhwc_kernel(const T* x, T* xp, int64_t C, int64_t H,
+                                                        int64_t W, int64_t pad) {
+  constexpr int E = 16 / (int)sizeof(T);
+  __shared__ __attribute__((aligned(16))) T tile[64][64 + E];
   const int64_t Hp = H + 2 * pad, Wp = W + 2 * pad, HWp = Hp * Wp;
   const int64_t pos0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64, n = blockIdx.z;
   const int t = threadIdx.x;
@@ -30,7 +72,7 @@ __global__ __launch_bounds__(256) void pack_nhwc_kernel(const bf16* x, bf16* xp,
   for (int it = 0; it < 16; ++it) {
     const int idx = it * 256 + t, cl = idx >> 6, pl = idx & 63;
     const int64_t pos = pos0 + pl, c = c0 + cl;
-    bf16 v = 0;
+    T v = T(0);
     if (pos < HWp && c < C) {
       const int64_t h = pos / Wp - pad, w = pos % Wp - pad;
       if (h >= 0 && h < H && w >= 0 && w < W) v = x[((n * C + c) * H + h) * W + w];
@@ -38,18 +80,18 @@ __global__ __launch_bounds__(256) void pack_nhwc_kernel(const bf16* x, bf16* xp,
     tile[pl][cl] = v;
   }
   __syncthreads();
-#pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    const int idx = it * 256 + t, pl = idx >> 3, ch = idx & 7;
-    const int64_t pos = pos0 + pl, c = c0 + ch * 8;
+  constexpr int CPP = 64 / E;
+  for (int idx = t; idx < 64 * CPP; idx += 256) {
+    const int pl = idx / CPP, ch = idx % CPP;
+    const int64_t pos = pos0 + pl, c = c0 + ch * E;
     if (pos < HWp && c < C)
-      *(uint4*)(xp + (n * HWp + pos) * C + c) = *(const uint4*)&tile[pl][ch * 8];
+      *(uint4*)(xp + (n * HWp + pos) * C + c) = *(const uint4*)&tile[pl][ch * E];
   }
 }
 
 // w [K][C][R][S] -> wp [K][R][S][C].
-__global__ void pack_krsc_kernel(const bf16* w, bf16* wp, int64_t K, int64_t C, int64_t R,
-                                 int64_t S) {
+template <typename T>
+__global__ void pack_krsc_kernel(const T* w, T* wp, int64_t K, int64_t C, int64_t R, int64_t S) {
   const int64_t total = K * R * S * C;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * blockDim.x) {
@@ -60,9 +102,10 @@ __global__ void pack_krsc_kernel(const bf16* w, bf16* wp, int64_t K, int64_t C, 
 
 // out[n][k] = (sum of the GAP partials of the position tiles that cover image
 // n, in tile order) / PQ.  Partial (tile t, slot) holds the column sums of the
-// tile's positions in image (t*256)/PQ + slot.
+// tile's positions in image (t*tile)/PQ + slot.
+template <typename T>
 __global__ void gap_finish_kernel(const float* partial, int64_t N, int64_t K, int64_t PQ,
-                                  int64_t tile, bf16* out) {
+                                  int64_t tile, T* out) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= N * K) return;
   const int64_t n = i / K, k = i % K;
@@ -72,41 +115,64 @@ __global__ void gap_finish_kernel(const float* partial, int64_t N, int64_t K, in
     const int64_t slot = n - (t * tile) / PQ;
     s += partial[(t * 2 + slot) * K + k];
   }
-  out[i] = f2bf(s / (float)PQ);
+  st<T>(out, i, s / (float)PQ);
 }
 
 }  // namespace
 
+static int64_t esize(int dtype) { return dtype == MK_BF16 ? 2 : 4; }
+
 bool conv_mfma_supported(int dtype, const ConvArgs& a) {
-  if (dtype != MK_BF16 || a.C % 32 || (a.P * a.Q) % 8) return false;
+  if (dtype != MK_BF16 && dtype != MK_F32) return false;
+  // A K slice (32 bf16 / 16 fp32 channels of one (r, s)) must not cross an
+  // (r, s) boundary; 8 consecutive positions stay in one image.
+  const int64_t bk = dtype == MK_BF16 ? 32 : 16;
+  if (a.C % bk || (a.P * a.Q) % 8) return false;
   if (a.gap && a.P * a.Q < kConvTileN) return false;   // a tile spans at most two images
-  const int64_t xp = a.N * (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C * 2;
-  return xp < ((int64_t)1 << 31) && a.K * a.R * a.S * a.C * 2 < ((int64_t)1 << 31);
+  const int64_t xp = a.N * (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C * esize(dtype);
+  return xp < ((int64_t)1 << 31) && a.K * a.R * a.S * a.C * esize(dtype) < ((int64_t)1 << 31);
 }
 
-ConvScratch conv_mfma_scratch(const ConvArgs& a) {
+ConvScratch conv_mfma_scratch(int dtype, const ConvArgs& a) {
   ConvScratch s{};
   auto al = [](int64_t b) { return (b + 255) / 256 * 256; };
-  s.xp_bytes = al(a.N * (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C * 2);
-  s.wp_bytes = al(a.K * a.R * a.S * a.C * 2);
+  s.xp_bytes = al(a.N * (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C * esize(dtype));
+  s.wp_bytes = al(a.K * a.R * a.S * a.C * esize(dtype));
   const int64_t tiles = (a.N * a.P * a.Q + kConvTileN - 1) / kConvTileN;
   s.partial_bytes = a.gap ? al(tiles * 2 * a.K * 4) : 0;
   return s;
 }
 
-hipError_t launch_pack_nhwc(const ConvArgs& a, void* xp, hipStream_t st) {
-  const int64_t HWp = (a.H + 2 * a.pad) * (a.W + 2 * a.pad);
-  dim3 grid((unsigned)((HWp + 63) / 64), (unsigned)((a.C + 63) / 64), (unsigned)a.N);
-  hipLaunchKernelGGL(pack_nhwc_kernel, grid, dim3(256), 0, st, (const bf16*)a.x, (bf16*)xp, a.C,
-                     a.H, a.W, a.pad);
+template <typename T>
+static void launch_pack_nhwc_t(const ConvArgs& a, void* xp, hipStream_t st) {
+  constexpr int E = 16 / (int)sizeof(T);
+  const int64_t Hp = a.H + 2 * a.pad, HWp = Hp * (a.W + 2 * a.pad);
+  const unsigned cb = (unsigned)((a.C + 63) / 64);
+  if (a.W <= 64 && a.W % E == 0 && (uintptr_t)a.x % 16 == 0)
+    hipLaunchKernelGGL(pack_nhwc_rows_kernel<T>, dim3((unsigned)Hp, cb, (unsigned)a.N), dim3(256),
+                       0, st, (const T*)a.x, (T*)xp, a.C, a.H, a.W, a.pad);
+  else
+    hipLaunchKernelGGL(pack_nhwc_kernel<T>, dim3((unsigned)((HWp + 63) / 64), cb, (unsigned)a.N),
+                       dim3(256), 0, st, (const T*)a.x, (T*)xp, a.C, a.H, a.W, a.pad);
+}
+
+hipError_t launch_pack_nhwc(int dtype, const ConvArgs& a, void* xp, hipStream_t st) {
+  if (dtype == MK_BF16)
+    launch_pack_nhwc_t<bf16>(a, xp, st);
+  else
+    launch_pack_nhwc_t<float>(a, xp, st);
   return hipGetLastError();
 }
 
-hipError_t launch_pack_krsc(const ConvArgs& a, void* wp, hipStream_t st) {
+hipError_t launch_pack_krsc(int dtype, const ConvArgs& a, void* wp, hipStream_t st) {
   const int64_t total = a.K * a.R * a.S * a.C;
   const unsigned g = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
-  hipLaunchKernelGGL(pack_krsc_kernel, dim3(g), dim3(256), 0, st, (const bf16*)a.w, (bf16*)wp,
-                     a.K, a.C, a.R, a.S);
+  if (dtype == MK_BF16)
+    hipLaunchKernelGGL(pack_krsc_kernel<bf16>, dim3(g), dim3(256), 0, st, (const bf16*)a.w,
+                       (bf16*)wp, a.K, a.C, a.R, a.S);
+  else
+    hipLaunchKernelGGL(pack_krsc_kernel<float>, dim3(g), dim3(256), 0, st, (const float*)a.w,
+                       (float*)wp, a.K, a.C, a.R, a.S);
   return hipGetLastError();
 }
 
@@ -139,10 +205,15 @@ GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float
   return g;
 }
 
-hipError_t launch_gap_finish(const ConvArgs& a, const float* partial, hipStream_t st) {
+hipError_t launch_gap_finish(int dtype, const ConvArgs& a, const float* partial, hipStream_t st) {
   const int64_t total = a.N * a.K;
-  hipLaunchKernelGGL(gap_finish_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st,
-                     partial, a.N, a.K, a.P * a.Q, kConvTileN, (bf16*)a.y);
+  const dim3 grid((unsigned)((total + 255) / 256));
+  if (dtype == MK_BF16)
+    hipLaunchKernelGGL(gap_finish_kernel<bf16>, grid, dim3(256), 0, st, partial, a.N, a.K,
+                       a.P * a.Q, (int64_t)kConvTileN, (bf16*)a.y);
+  else
+    hipLaunchKernelGGL(gap_finish_kernel<float>, grid, dim3(256), 0, st, partial, a.N, a.K,
+                       a.P * a.Q, (int64_t)kConvTileN, (float*)a.y);
   return hipGetLastError();
 }
 

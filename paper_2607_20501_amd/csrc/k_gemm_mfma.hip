@@ -41,12 +41,29 @@
 namespace mk {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 namespace {
 
-constexpr int BM = 256, BK = 32;
-constexpr int kTileBytes = BM * BK * 2;           // 16 KB A slice
+// A K slice is 64 bytes of every operand row: 32 bf16 or 16 fp32 values,
+// four 16-byte chunks.  MfmaType<T> gives the slice depth and the fragment.
+template <typename T>
+struct MfmaType;
+template <>
+struct MfmaType<bf16> {
+  static constexpr int BK = 32;
+  typedef bf16x8 frag;      // 8 consecutive k of one row / column
+};
+template <>
+struct MfmaType<float> {
+  static constexpr int BK = 16;
+  typedef f32x4 frag;       // 4 consecutive k
+};
+
+constexpr int BM = 256;
+constexpr int kRowBytes = 64;                     // one K slice of one row
+constexpr int kTileBytes = BM * kRowBytes;        // 16 KB A slice
 constexpr int kGroupM = 8;                        // tile rows per locality group
 constexpr int kXcds = 8;
 
@@ -96,15 +113,16 @@ typedef __attribute__((address_space(3))) void lds_void;
 // 16-byte chunks).  For
 // load q of wave w, lane i fills LDS chunk p = (q*WAVES + w)*64 + i, i.e. row
 // p/4, physical chunk p%4, whose logical chunk is (p%4) ^ swz(row).
-template <int WAVES, int ROWS>
+template <int WAVES, int ROWS, typename T>
 struct SliceLoader {
+  static constexpr int E = 16 / (int)sizeof(T);        // elements per chunk
   static constexpr int LQ = ROWS * 4 / (64 * WAVES);   // loads per thread per slice
   __amdgpu_buffer_rsrc_t src;
   uint32_t voff[LQ];   // byte offset at k0 = 0, kOob if the row is out of range
   int lchunk[LQ];      // logical 16-byte chunk of this lane's loads
 
-  __device__ __forceinline__ void init(const bf16* base, int64_t rows, int64_t ld, int64_t r0) {
-    src = make_rsrc(base, rows * ld * 2);
+  __device__ __forceinline__ void init(const T* base, int64_t rows, int64_t ld, int64_t r0) {
+    src = make_rsrc(base, rows * ld * (int64_t)sizeof(T));
     const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
     for (int q = 0; q < LQ; ++q) {
@@ -113,14 +131,14 @@ struct SliceLoader {
       const int c = (p & 3) ^ swz(row);
       lchunk[q] = c;
       const int64_t g = r0 + row;
-      voff[q] = g < rows ? (uint32_t)(g * ld * 2 + c * 16) : kOob;
+      voff[q] = g < rows ? (uint32_t)(g * ld * (int64_t)sizeof(T) + c * 16) : kOob;
     }
   }
 
   // Rows gathered from arbitrary byte offsets (implicit-GEMM conv: output
   // position m -> its window origin in the padded NHWC input).
   template <typename RowOff>
-  __device__ __forceinline__ void init_gather(const bf16* base, int64_t bytes, int64_t rows,
+  __device__ __forceinline__ void init_gather(const T* base, int64_t bytes, int64_t rows,
                                               int64_t r0, RowOff rowoff) {
     src = make_rsrc(base, bytes);
     const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -142,43 +160,56 @@ struct SliceLoader {
     const int64_t krem = K - k0;
 #pragma unroll
     for (int q = 0; q < LQ; ++q) {
-      const uint32_t off = lchunk[q] * 8 < krem ? voff[q] : kOob;
+      const uint32_t off = lchunk[q] * E < krem ? voff[q] : kOob;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * WAVES + w) * 1024),
                                                16, (int)off, (int)soff, 0, 0);
     }
   }
   __device__ __forceinline__ void issue(char* dst, int64_t k0, int64_t K) const {
-    issue(dst, k0, K, (uint32_t)(k0 * 2));
+    issue(dst, k0, K, (uint32_t)(k0 * (int64_t)sizeof(T)));
   }
 };
 
-// MFMA operand fragments of one 16-deep k step for this wave: 4 row tiles of
-// A and NJ column tiles of B (32 x 16 bf16 each).
-template <int NJ>
+// MFMA operand fragments of one half slice (chunks 2kk, 2kk+1) for this
+// wave: 4 row tiles of A and NJ column tiles of B; lane (lr, lh) holds the
+// 16-byte chunk 2kk+lh of row / column lr of each tile.
+template <int NJ, typename T>
 struct Frags {
-  bf16x8 a[4], b[NJ];
+  typename MfmaType<T>::frag a[4], b[NJ];
 };
 
-template <int NJ>
+template <int NJ, typename T>
 __device__ __forceinline__ void load_frags(const char* stage, int kk, int rowbase, int colbase,
-                                           int lr, int lh, Frags<NJ>& f) {
+                                           int lr, int lh, Frags<NJ, T>& f) {
+  typedef typename MfmaType<T>::frag F;
   const char* la = stage;
   const char* lb = stage + kTileBytes;   // B slice follows the 256-row A slice
 #pragma unroll
   for (int i = 0; i < 4; ++i)
-    f.a[i] = *(const bf16x8*)(la + lds_off(rowbase + i * 32 + lr, kk * 2 + lh));
+    f.a[i] = *(const F*)(la + lds_off(rowbase + i * 32 + lr, kk * 2 + lh));
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
-    f.b[j] = *(const bf16x8*)(lb + lds_off(colbase + j * 32 + lr, kk * 2 + lh));
+    f.b[j] = *(const F*)(lb + lds_off(colbase + j * 32 + lr, kk * 2 + lh));
 }
 
-template <int NJ>
-__device__ __forceinline__ void mfma_step(const Frags<NJ>& f, f32x16 (&acc)[4][NJ]) {
+// bf16: one 32x32x16 MFMA per tile pair (the lane's 8 k values are the
+// instruction's k = 8*lh .. 8*lh+7).  fp32: the lane's 4 k values feed four
+// 32x32x2 MFMAs, instruction t taking k = 4*lh + t of the chunk pair; A and B
+// use the same assignment, so the sum over k is unchanged.
+template <int NJ, typename T>
+__device__ __forceinline__ void mfma_step(const Frags<NJ, T>& f, f32x16 (&acc)[4][NJ]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+    for (int j = 0; j < NJ; ++j) {
+      if constexpr (sizeof(T) == 2) {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.a[i][t], f.b[j][t], acc[i][j], 0, 0, 0);
+      }
+    }
 }
 
 // vmcnt(n) with the other counters left alone (gfx9 encoding).
@@ -203,22 +234,24 @@ __device__ __forceinline__ void stage_slab(const f32x16 (&acc)[4][NJ], float* sl
 // WN waves along N (2: four waves of 128 x 128; 4: eight waves of 128 x 64,
 // two per SIMD so one wave's MFMAs cover the other's waits).
 // Byte offset along K of implicit-GEMM slice k0 (k = (r*S + s)*C + c, and a
-// 32-deep slice never crosses an (r, s) boundary since C % 32 == 0).
+// slice never crosses an (r, s) boundary since C is a multiple of its depth).
+template <typename T>
 __device__ __forceinline__ uint32_t conv_koff(const GemmArgs& a, int64_t k0) {
   const int64_t rs = k0 / a.cv_C, c0 = k0 % a.cv_C;
   const int64_t r = rs / a.cv_S, s = rs % a.cv_S;
-  return (uint32_t)(((r * a.cv_Wp + s) * a.cv_C + c0) * 2);
+  return (uint32_t)(((r * a.cv_Wp + s) * a.cv_C + c0) * (int64_t)sizeof(T));
 }
 
 // Variants: WN waves along N (2 rows of waves), BN columns per tile, STG
 // ring stages.  <4, 256, 4>: eight waves share one 256 x 256 tile (one
 // workgroup per CU).  <2, 128, 3>: four waves on a 256 x 128 tile in 72 KB of
 // LDS, so two independent workgroups share each CU.
-template <int WN, int BN, int STG, int CONV, int PIPE>
-__global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_kernel(GemmArgs a) {
+template <typename T, int WN, int BN, int STG, int CONV, int PIPE>
+__global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kernel(GemmArgs a) {
+  constexpr int BK = MfmaType<T>::BK;
   constexpr int WAVES = 2 * WN, THREADS = 64 * WAVES;
   constexpr int kStages = STG;
-  constexpr int kStageBytes = (BM + BN) * BK * 2;
+  constexpr int kStageBytes = (BM + BN) * kRowBytes;
   constexpr int WTN = BN / WN;        // wave tile columns
   constexpr int NJ = WTN / 32;        // 32-wide column tiles per wave
   constexpr int LD = WTN + 8;         // epilogue slab row stride (floats)
@@ -229,8 +262,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
   const TileCoord tc = tile_of(blockIdx.x, tiles_m, tiles_n);
   const int64_t m0 = (int64_t)tc.tm * BM, n0 = (int64_t)tc.tn * BN;
   const int64_t z = blockIdx.y, bb = z / a.heads, hh = z % a.heads;
-  const bf16* A = (const bf16*)a.A + a.a_off + bb * a.a_sb + hh * a.a_sh;
-  const bf16* B = (const bf16*)a.B + a.b_off + bb * a.b_sb + hh * a.b_sh;
+  const T* A = (const T*)a.A + a.a_off + bb * a.a_sb + hh * a.a_sh;
+  const T* B = (const T*)a.B + a.b_off + bb * a.b_sb + hh * a.b_sh;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / WN, wn = w % WN;
@@ -246,23 +279,24 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = (int)((a.K + BK - 1) / BK);
-  SliceLoader<WAVES, BM> la;
-  SliceLoader<WAVES, BN> lb;
+  SliceLoader<WAVES, BM, T> la;
+  SliceLoader<WAVES, BN, T> lb;
   la.init(A, a.M, a.lda, m0);
   const int64_t PQ = a.cv_P * a.cv_Q;
   if (CONV) {
-    const int64_t bytes = a.cv_Hp * a.cv_Wp * a.cv_C * 2 * (a.N / PQ);
+    const int64_t bytes = a.cv_Hp * a.cv_Wp * a.cv_C * (int64_t)sizeof(T) * (a.N / PQ);
     lb.init_gather(B, bytes, a.N, n0, [&](int64_t m) {
       const int64_t n = m / PQ, pq = m % PQ;
       const int64_t p = pq / a.cv_Q, q = pq % a.cv_Q;
-      return ((n * a.cv_Hp + p * a.cv_stride) * a.cv_Wp + q * a.cv_stride) * a.cv_C * 2;
+      return ((n * a.cv_Hp + p * a.cv_stride) * a.cv_Wp + q * a.cv_stride) * a.cv_C *
+             (int64_t)sizeof(T);
     });
   } else {
     lb.init(B, a.N, a.ldb, n0);
   }
   auto issue_b = [&](char* dst, int64_t k0) {
     if (CONV)
-      lb.issue(dst, k0, a.K, conv_koff(a, k0));
+      lb.issue(dst, k0, a.K, conv_koff<T>(a, k0));
     else
       lb.issue(dst, k0, a.K);
   };
@@ -273,7 +307,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
       issue_b(smem + s * kStageBytes + kTileBytes, (int64_t)s * BK);
     }
 
-  constexpr int LPS = SliceLoader<WAVES, BM>::LQ + SliceLoader<WAVES, BN>::LQ;
+  constexpr int LPS = SliceLoader<WAVES, BM, T>::LQ + SliceLoader<WAVES, BN, T>::LQ;
   // Wait until at most `later` slices issued after the one needed are still
   // in flight (each slice is LPS loads of this wave, issued in order).
   auto wait_slices = [](int later) {
@@ -295,14 +329,14 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
     // slot takes slice kt+STG-1.
     wait_slices(min(kStages - 2, nk - 1));
     __builtin_amdgcn_s_barrier();
-    Frags<NJ> f0, f1;
-    load_frags<NJ>(smem, 0, rowbase, colbase, lr, lh, f0);
+    Frags<NJ, T> f0, f1;
+    load_frags<NJ, T>(smem, 0, rowbase, colbase, lr, lh, f0);
     // (The last step is peeled so the loop body has no branch between the
     // two groups of reads, which lets each MFMA group wait only for its own.)
     for (int kt = 0; kt < nk - 1; ++kt) {
-      load_frags<NJ>(smem + (kt % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
+      load_frags<NJ, T>(smem + (kt % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
       __builtin_amdgcn_sched_barrier(0);
-      mfma_step<NJ>(f0, acc);
+      mfma_step<NJ, T>(f0, acc);
       __builtin_amdgcn_sched_barrier(0);
       wait_slices(min(kStages - 3, nk - 2 - kt));
       __builtin_amdgcn_s_barrier();
@@ -312,15 +346,15 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
         la.issue(st, (int64_t)nxt * BK, a.K);
         issue_b(st + kTileBytes, (int64_t)nxt * BK);
       }
-      load_frags<NJ>(smem + ((kt + 1) % kStages) * kStageBytes, 0, rowbase, colbase, lr, lh, f0);
+      load_frags<NJ, T>(smem + ((kt + 1) % kStages) * kStageBytes, 0, rowbase, colbase, lr, lh, f0);
       __builtin_amdgcn_sched_barrier(0);
-      mfma_step<NJ>(f1, acc);
+      mfma_step<NJ, T>(f1, acc);
       __builtin_amdgcn_sched_barrier(0);
     }
-    load_frags<NJ>(smem + ((nk - 1) % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
+    load_frags<NJ, T>(smem + ((nk - 1) % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_step<NJ>(f0, acc);
-    mfma_step<NJ>(f1, acc);
+    mfma_step<NJ, T>(f0, acc);
+    mfma_step<NJ, T>(f1, acc);
   } else {
     for (int kt = 0; kt < nk; ++kt) {
       // Slice kt has landed once at most the loads of the later slices are
@@ -338,13 +372,13 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
         issue_b(st + kTileBytes, (int64_t)nxt * BK);
       }
       const char* cur = smem + (kt % kStages) * kStageBytes;
-      Frags<NJ> f0, f1;
-      load_frags<NJ>(cur, 0, rowbase, colbase, lr, lh, f0);
-      load_frags<NJ>(cur, 1, rowbase, colbase, lr, lh, f1);
+      Frags<NJ, T> f0, f1;
+      load_frags<NJ, T>(cur, 0, rowbase, colbase, lr, lh, f0);
+      load_frags<NJ, T>(cur, 1, rowbase, colbase, lr, lh, f1);
       __builtin_amdgcn_sched_barrier(0);
-      mfma_step<NJ>(f0, acc);
+      mfma_step<NJ, T>(f0, acc);
       __builtin_amdgcn_sched_barrier(0);
-      mfma_step<NJ>(f1, acc);
+      mfma_step<NJ, T>(f1, acc);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -360,7 +394,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
   float* slab = (float*)smem + w * (32 * LD);
   float* red = (float*)smem + WAVES * 32 * LD;   // [WN column groups][256 rows][2]
   const int64_t cbase = a.c_off + bb * a.c_sb + hh * a.c_sh;
-  bf16* C = (bf16*)a.C + cbase;
+  T* C = (T*)a.C + cbase;
   const bool softmax = a.terminal == TERM_SOFTMAX;
   const int q = lane % LPR;          // 8-column group within the slab row
   const int64_t col0 = n0 + colbase + q * 8;
@@ -388,10 +422,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
       const int64_t obase = CONV ? (img * a.M + row) * PQ + (col0 - img * PQ)
                                  : cbase + row * a.ldc + col0;
       if (a.epi.n && row_ok && valid > 0)
-        epi_apply8<bf16>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok));
+        epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok));
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX) v[e] = bf2f(f2bf(v[e]));
+        if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX) v[e] = rnd<T>(v[e]);
         if (e < valid) {
           m = fmaxf(m, v[e]);
           sum += v[e];
@@ -421,35 +455,15 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
         continue;
       }
       if (a.terminal != TERM_ROWSUM && row_ok) {
-        if (CONV) {
-          if (valid == 8) {
-            uint4 o;
-            o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-            o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-            o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
-            o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
-            *(uint4*)(C + obase) = o;
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (e < valid) C[obase + e] = f2bf(v[e]);
-          }
-        } else if (valid == 8) {
-          uint4 o;
-          o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-          o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-          o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
-          o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
-          if (vec_ok) {
-            *(uint4*)(C + row * a.ldc + col0) = o;
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) C[row * a.ldc + col0 + e] = f2bf(v[e]);
-          }
+        // NCHW conv output is always 8-aligned (PQ % 8 == 0); a row-major
+        // output needs ldc and the batch offset 8-aligned for the vector store.
+        const int64_t off = CONV ? obase : row * a.ldc + col0;
+        if (valid == 8 && (CONV || vec_ok)) {
+          st8<T>(C + off, v);
         } else {
 #pragma unroll
           for (int e = 0; e < 8; ++e)
-            if (e < valid) C[row * a.ldc + col0 + e] = f2bf(v[e]);
+            if (e < valid) st<T>(C, off + e, v[e]);
         }
       }
       if (a.terminal != TERM_NONE) {
@@ -526,33 +540,35 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_bf16_mfma_
 
 // B(k, n) of a [K, N] operand (batched) -> dst[z][n][k], K contiguous.  One
 // 64 x 64 tile per workgroup through LDS; 16-byte global accesses on both
-// sides (K and N are multiples of 8).
-__global__ __launch_bounds__(256) void transpose_b_kernel(GemmArgs a, bf16* dst) {
-  __shared__ bf16 tile[64][72];
+// sides (K and N are multiples of the 16-byte chunk).
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_b_kernel(GemmArgs a, T* dst) {
+  constexpr int E = 16 / (int)sizeof(T);    // elements per chunk
+  constexpr int CPR = 64 / E;               // chunks per 64-element tile row
+  constexpr int RPP = 256 / CPR;            // tile rows per pass
+  __shared__ __attribute__((aligned(16))) T tile[64][64 + E];
   const int64_t z = blockIdx.z, bb = z / a.heads, hh = z % a.heads;
-  const bf16* src = (const bf16*)a.B + a.b_off + bb * a.b_sb + hh * a.b_sh;
+  const T* src = (const T*)a.B + a.b_off + bb * a.b_sb + hh * a.b_sh;
   const int64_t k0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
-  const int t = threadIdx.x, r = t >> 3, c8 = (t & 7) * 8;
+  const int t = threadIdx.x, r = t / CPR, ce = (t % CPR) * E;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int64_t k = k0 + r + h * 32, n = n0 + c8;
+  for (int h = 0; h < 64 / RPP; ++h) {
+    const int64_t k = k0 + r + h * RPP, n = n0 + ce;
     uint4 v = make_uint4(0, 0, 0, 0);
     if (k < a.K && n < a.N) v = *(const uint4*)(src + k * a.ldb + n);
-    *(uint4*)&tile[r + h * 32][c8] = v;
+    *(uint4*)&tile[r + h * RPP][ce] = v;
   }
   __syncthreads();
-  bf16* out = dst + z * a.N * a.K;
+  T* out = dst + z * a.N * a.K;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int nl = r + h * 32;
-    const int64_t n = n0 + nl, k = k0 + c8;
+  for (int h = 0; h < 64 / RPP; ++h) {
+    const int nl = r + h * RPP;
+    const int64_t n = n0 + nl, k = k0 + ce;
     if (n < a.N && k < a.K) {
-      uint4 v;
-      v.x = (uint32_t)tile[c8 + 0][nl] | ((uint32_t)tile[c8 + 1][nl] << 16);
-      v.y = (uint32_t)tile[c8 + 2][nl] | ((uint32_t)tile[c8 + 3][nl] << 16);
-      v.z = (uint32_t)tile[c8 + 4][nl] | ((uint32_t)tile[c8 + 5][nl] << 16);
-      v.w = (uint32_t)tile[c8 + 6][nl] | ((uint32_t)tile[c8 + 7][nl] << 16);
-      *(uint4*)(out + n * a.K + k) = v;
+      T v[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) v[e] = tile[ce + e][nl];
+      *(uint4*)(out + n * a.K + k) = __builtin_bit_cast(uint4, v);
     }
   }
 }
@@ -560,31 +576,35 @@ __global__ __launch_bounds__(256) void transpose_b_kernel(GemmArgs a, bf16* dst)
 }  // namespace
 
 bool gemm_mfma_supported(int dtype, const GemmArgs& a) {
-  if (dtype != MK_BF16) return false;
+  if (dtype != MK_BF16 && dtype != MK_F32) return false;
+  const int64_t es = dtype == MK_BF16 ? 2 : 4, E = 16 / es;
   // 16-byte operand chunks: K (and N for a [K, N] weight), leading dimensions
-  // and batch offsets must be multiples of 8 elements.
-  if (a.K % 8 || a.lda % 8 || a.ldb % 8) return false;
-  if (a.layout == 1 && a.N % 8) return false;
+  // and batch offsets must be multiples of the chunk.
+  if (a.K % E || a.lda % E || a.ldb % E) return false;
+  if (a.layout == 1 && a.N % E) return false;
   const int64_t offs[] = {a.a_off, a.a_sb, a.a_sh, a.b_off, a.b_sb, a.b_sh};
   for (int64_t o : offs)
-    if (o % 8) return false;
+    if (o % E) return false;
   if (a.M < 1 || a.N < 1 || a.K < 1) return false;
   if (a.terminal != TERM_NONE && a.batch * a.heads != 1) return false;
   // Buffer-resource ranges are 32-bit: every operand slice must stay below 2 GB.
   const int64_t lim = (int64_t)1 << 31;
-  if (a.M * a.lda * 2 >= lim || a.N * (a.layout == 0 ? a.ldb : a.K) * 2 >= lim) return false;
+  if (a.M * a.lda * es >= lim || a.N * (a.layout == 0 ? a.ldb : a.K) * es >= lim) return false;
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + 127) / 128);
   return tiles < (1ll << 31) && a.batch * a.heads <= 65535;
 }
 
-int64_t gemm_mfma_bt_bytes(const GemmArgs& a) {
-  return a.layout == 1 ? (int64_t)a.batch * a.heads * a.N * a.K * 2 : 0;
+int64_t gemm_mfma_bt_bytes(int dtype, const GemmArgs& a) {
+  return a.layout == 1 ? (int64_t)a.batch * a.heads * a.N * a.K * (dtype == MK_BF16 ? 2 : 4) : 0;
 }
 
-hipError_t launch_transpose_b(const GemmArgs& a, void* dst, hipStream_t st) {
+hipError_t launch_transpose_b(int dtype, const GemmArgs& a, void* dst, hipStream_t st) {
   dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)((a.K + 63) / 64),
             (unsigned)(a.batch * a.heads));
-  hipLaunchKernelGGL(transpose_b_kernel, grid, dim3(256), 0, st, a, (bf16*)dst);
+  if (dtype == MK_BF16)
+    hipLaunchKernelGGL(transpose_b_kernel<bf16>, grid, dim3(256), 0, st, a, (bf16*)dst);
+  else
+    hipLaunchKernelGGL(transpose_b_kernel<float>, grid, dim3(256), 0, st, a, (float*)dst);
   return hipGetLastError();
 }
 
@@ -599,26 +619,34 @@ GemmArgs gemm_with_bt(const GemmArgs& a, const void* bt) {
   return g;
 }
 
+template <typename T>
+static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
+  // (The conv variant keeps the plain loop: with three stages the pipelined
+  // one would leave only one step of load latency hiding.)
+  if (a.conv)
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kConvTileN, 3, 1, 0>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 4, 0, 1>), grid, dim3(512), 0, st, a);
+}
+
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
+  const int E = dtype == MK_BF16 ? 8 : 4;
   if (a.conv) {
-    if (dtype != MK_BF16 || a.cv_C % 32 || (a.cv_P * a.cv_Q) % 8 || a.lda % 8 || a.K % 32)
+    const int BKe = dtype == MK_BF16 ? 32 : 16;   // slice depth
+    if ((dtype != MK_BF16 && dtype != MK_F32) || a.cv_C % BKe || (a.cv_P * a.cv_Q) % 8 ||
+        a.lda % E || a.K % BKe)
       return hipErrorInvalidValue;
   } else if (!gemm_mfma_supported(dtype, a) || a.layout != 0) {
     return hipErrorInvalidValue;
   }
   if (((uintptr_t)a.A | (uintptr_t)a.B) % 16) return hipErrorInvalidValue;
-  // Plain GEMMs: 256 x 256 tiles, 8 waves, 4-stage ring.  Conv GEMMs: 256 x 128
-  // tiles, 4 waves, 3 stages -- the gathered B rows make the wider tile's
-  // address set-up cost more than its extra reuse saves.
   const int64_t bn = a.conv ? kConvTileN : kGemmTileN;
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + bn - 1) / bn);
   dim3 grid((unsigned)tiles, (unsigned)(a.batch * a.heads));
-  // (The conv variant keeps the plain loop: with three stages the pipelined
-  // one would leave only one step of load latency hiding.)
-  if (a.conv)
-    hipLaunchKernelGGL((gemm_bf16_mfma_kernel<2, kConvTileN, 3, 1, 0>), grid, dim3(256), 0, st, a);
+  if (dtype == MK_BF16)
+    launch_gemm_t<bf16>(a, grid, st);
   else
-    hipLaunchKernelGGL((gemm_bf16_mfma_kernel<4, kGemmTileN, 4, 0, 1>), grid, dim3(512), 0, st, a);
+    launch_gemm_t<float>(a, grid, st);
   return hipGetLastError();
 }
 

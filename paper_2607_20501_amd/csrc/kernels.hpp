@@ -105,12 +105,12 @@ hipError_t launch_ew_fast(int dtype, const EwArgs& a, hipStream_t st);
 // per-tile partial layouts of the terminal finishers follow them.
 constexpr int kGemmTileN = 256;
 constexpr int kConvTileN = 128;
-bool gemm_mfma_supported(int dtype, const GemmArgs& a);
+bool gemm_mfma_supported(int dtype, const GemmArgs& a);   // bf16 or fp32
 // The MFMA kernel takes B as [N, K]; a [K, N] operand (layout 1) is first
 // transposed into scratch of gemm_mfma_bt_bytes() bytes, and gemm_with_bt()
 // gives the arguments that read it there.
-int64_t gemm_mfma_bt_bytes(const GemmArgs& a);
-hipError_t launch_transpose_b(const GemmArgs& a, void* dst, hipStream_t st);
+int64_t gemm_mfma_bt_bytes(int dtype, const GemmArgs& a);
+hipError_t launch_transpose_b(int dtype, const GemmArgs& a, void* dst, hipStream_t st);
 GemmArgs gemm_with_bt(const GemmArgs& a, const void* bt);
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st);
 // Implicit-GEMM conv: pack_nhwc (x -> zero-padded NHWC), pack_krsc (w ->
@@ -120,11 +120,11 @@ struct ConvScratch {
   int64_t xp_bytes, wp_bytes, partial_bytes;
 };
 bool conv_mfma_supported(int dtype, const ConvArgs& a);
-ConvScratch conv_mfma_scratch(const ConvArgs& a);
-hipError_t launch_pack_nhwc(const ConvArgs& a, void* xp, hipStream_t st);
-hipError_t launch_pack_krsc(const ConvArgs& a, void* wp, hipStream_t st);
+ConvScratch conv_mfma_scratch(int dtype, const ConvArgs& a);
+hipError_t launch_pack_nhwc(int dtype, const ConvArgs& a, void* xp, hipStream_t st);
+hipError_t launch_pack_krsc(int dtype, const ConvArgs& a, void* wp, hipStream_t st);
 GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float* partial);
-hipError_t launch_gap_finish(const ConvArgs& a, const float* partial, hipStream_t st);
+hipError_t launch_gap_finish(int dtype, const ConvArgs& a, const float* partial, hipStream_t st);
 bool attn_fused_supported(int dtype, const AttnArgs& a);
 hipError_t launch_attn_fused(int dtype, const AttnArgs& a, hipStream_t st);
 

@@ -55,7 +55,8 @@ class mk_subkernel_info_t(ctypes.Structure):
                 ("out_bytes", ctypes.c_int64), ("ws_offset", ctypes.c_int64),
                 ("flops", ctypes.c_int64), ("alg_bytes", ctypes.c_int64),
                 ("family", ctypes.c_int32), ("impl", ctypes.c_int32),
-                ("n_launches", ctypes.c_int32), ("scratch_bytes", ctypes.c_int64)]
+                ("n_launches", ctypes.c_int32), ("scratch_bytes", ctypes.c_int64),
+                ("uses_mfma", ctypes.c_int32)]
 
 
 class mk_check(ctypes.Structure):
@@ -191,7 +192,7 @@ def mk_subkernel_info(h, i):
             "out_shape": _shape(s.out_shape), "out_bytes": s.out_bytes,
             "ws_offset": s.ws_offset, "flops": s.flops, "alg_bytes": s.alg_bytes,
             "family": FAMILIES[s.family], "impl": s.impl, "n_launches": s.n_launches,
-            "scratch_bytes": s.scratch_bytes}
+            "scratch_bytes": s.scratch_bytes, "uses_mfma": bool(s.uses_mfma)}
 
 
 def mk_subkernel_select(h, i, impl):

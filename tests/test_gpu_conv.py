@@ -1,6 +1,6 @@
-"""GPU parity of the conv family: implicit-GEMM MFMA path (bf16; padded-NHWC
-gather, NCHW store or fused GAP over tiles that straddle images) and the
-simple direct conv, against the oracle."""
+"""GPU parity of the conv family: implicit-GEMM MFMA path (bf16 and fp32;
+padded-NHWC gather, NCHW store or fused GAP over tiles that straddle images)
+and the simple direct conv, against the oracle."""
 import pytest
 import torch
 
@@ -17,12 +17,14 @@ CASES = [dict(N=3, C=32, H=20, W=20, K=40), dict(N=2, C=64, H=16, W=16, K=300),
          dict(N=2, C=8, H=9, W=7, K=5)]
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("shape", CASES)
 @pytest.mark.parametrize("dec", ["fused", "split"])
-def test_conv_parity(shape, dec):
-    print(f"conv {shape} {dec}", flush=True)
-    module = workloads.conv_relu_gap(**shape)
+def test_conv_parity(shape, dec, dtype):
+    print(f"conv {shape} {dec} {dtype}", flush=True)
+    module = workloads.conv_relu_gap(dtype=dtype, **shape)
     rep, m, *_ = run_parity(module, dec)
+    assert m.subkernels()[0]["uses_mfma"] == (shape["C"] % 32 == 0)
     assert rep["pass"], describe(rep)
 
 

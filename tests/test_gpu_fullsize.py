@@ -116,11 +116,12 @@ def test_mlp_block_full_size(decomp):
     assert ok, msg
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("decomp", ["fused", "split"])
-def test_conv_relu_gap_full_size(decomp):
-    module = workloads.full_size(3)
+def test_conv_relu_gap_full_size(decomp, dtype):
+    module = workloads.conv_relu_gap(dtype=dtype)
     print(f"full-size {module['name']} {decomp}", flush=True)
-    host = host_inputs(3, module)
+    host = host_inputs((3, dtype), module)
     out, groups = run_full(module, host, decomp)
     o32 = out.float()
     assert torch.isfinite(o32).all() and o32.min().item() >= 0
@@ -131,7 +132,7 @@ def test_conv_relu_gap_full_size(decomp):
     sub["inputs"][0] = [len(imgs), C, H, W]
     x = np.asarray(host[0]).reshape(N, -1)[imgs].reshape(-1)
     ref = oracle.run(sub, groups, [x] + list(host[1:]), keep={len(module["ops"]) - 1})[-1]
-    ok, msg = compare(mk.to_float64(out[imgs]), ref, "bf16")
+    ok, msg = compare(mk.to_float64(out[imgs]), ref, dtype)
     assert ok, msg
 
 

@@ -113,3 +113,41 @@ def test_split_and_fused_agree_with_their_own_references():
         assert rep["pass"], describe(rep)
         outs.append(mk.to_float64(out))
     np.testing.assert_allclose(outs[0], outs[1], rtol=5e-2, atol=2e-5)
+
+
+F32_SHAPES = [(256, 256, 64), (513, 264, 132), (300, 520, 200), (128, 256, 256),
+              (1000, 1024, 1028), (64, 4, 4)]
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+@pytest.mark.parametrize("shape", F32_SHAPES)
+def test_gemm_plain_f32(shape, layout):
+    """fp32 operands on the fp32 matrix cores (32x32x2 MFMA), ragged tails
+    included, to the fp32 tolerance."""
+    M, N, K = shape
+    print(f"gemm f32 {shape} layout {layout}", flush=True)
+    module = gemm_module(M, N, K, layout, dtype="f32")
+    rep, m, *_ = run_parity(module, [0])
+    assert m.subkernels()[0]["uses_mfma"]
+    assert rep["pass"], describe(rep)
+
+
+@pytest.mark.parametrize("term", ["SOFTMAX", "ROWSUM", None])
+def test_gemm_epilogue_f32(term):
+    epi = ("BIAS", "GELU_ERF", "SCALE") + ((term,) if term else ("ADD",))
+    module = gemm_module(333, 600, 196, 0, dtype="f32", epi=epi)
+    rep, m, *_ = run_parity(module, [0] * (len(epi) + 1))
+    assert m.subkernels()[0]["uses_mfma"]
+    assert rep["pass"], describe(rep)
+
+
+def test_linear_relu_rowsum_f32_both_impls():
+    """The fp32 Linear + bias + ReLU + row-sum module: tuned (MFMA) and simple
+    subkernels, fused and split."""
+    module = workloads.linear_relu_rowsum()
+    for dec in ("fused", "split"):
+        for impl in (mk.IMPL_TUNED, mk.IMPL_SIMPLE):
+            g = mk.mk_decomposition_preset(module, dec)
+            rep, m, *_ = run_parity(module, g, impls={i: impl for i in range(max(g) + 1)})
+            assert rep["pass"], f"{dec} impl {impl}: " + describe(rep)
+            assert m.subkernels()[0]["uses_mfma"] == (impl == mk.IMPL_TUNED)
