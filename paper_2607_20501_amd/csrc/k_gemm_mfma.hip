@@ -300,9 +300,11 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     else
       lb.issue(dst, k0, a.K);
   };
+  // The pipelined form issues all kStages - 1 leading slices even when K has
+  // fewer (the surplus ones read zeros), so its wait counts are exact.
 #pragma unroll
   for (int s = 0; s < kStages - 1; ++s)
-    if (s < nk) {
+    if (PIPE || s < nk) {
       la.issue(smem + s * kStageBytes, (int64_t)s * BK, a.K);
       issue_b(smem + s * kStageBytes + kTileBytes, (int64_t)s * BK);
     }
@@ -320,6 +322,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     else
       wait_vm<0>();
   };
+  // Per half slice and wave: MFMAs issued and fragment-read pairs.
+  constexpr int kMfmaHalf = 4 * NJ * (sizeof(T) == 2 ? 1 : 4);
+  constexpr int kReadPairs = (4 + NJ) / 2;
+  static_assert(PIPE != 2 || kMfmaHalf >= kReadPairs + LPS, "interleave needs more MFMAs");
   if (PIPE) {
     // Fragment reads run one half-step (k16) ahead of the MFMAs, so the
     // barrier sits between the two halves of a slice: the MFMAs of half 0 of
@@ -327,28 +333,47 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // half 0 of slice kt+1.  At the barrier of step kt every wave has
     // consumed slice kt-1 (its half-1 MFMAs waited on those reads), so that
     // slot takes slice kt+STG-1.
-    wait_slices(min(kStages - 2, nk - 1));
+    wait_vm<(kStages - 2) * LPS>();
     __builtin_amdgcn_s_barrier();
     Frags<NJ, T> f0, f1;
     load_frags<NJ, T>(smem, 0, rowbase, colbase, lr, lh, f0);
-    // (The last step is peeled so the loop body has no branch between the
-    // two groups of reads, which lets each MFMA group wait only for its own.)
+    // Branch-free body: the refill is issued every step; past the last
+    // slice every lane's offset is out of the descriptor's range, so it
+    // only writes zeros into the slot just consumed, which is never read
+    // again.  Exactly kStages - 3 slices are then in flight after the one
+    // needed, and the scheduler can spread the reads and loads between the
+    // MFMAs (one MFMA, then two reads, ...).
     for (int kt = 0; kt < nk - 1; ++kt) {
       load_frags<NJ, T>(smem + (kt % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
-      __builtin_amdgcn_sched_barrier(0);
       mfma_step<NJ, T>(f0, acc);
-      __builtin_amdgcn_sched_barrier(0);
-      wait_slices(min(kStages - 3, nk - 2 - kt));
-      __builtin_amdgcn_s_barrier();
-      const int nxt = kt + kStages - 1;
-      if (nxt < nk) {
-        char* st = smem + (nxt % kStages) * kStageBytes;
-        la.issue(st, (int64_t)nxt * BK, a.K);
-        issue_b(st + kTileBytes, (int64_t)nxt * BK);
+#pragma unroll
+      for (int g = 0; g < kReadPairs; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
       }
-      load_frags<NJ, T>(smem + ((kt + 1) % kStages) * kStageBytes, 0, rowbase, colbase, lr, lh, f0);
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaHalf - kReadPairs, 0);
       __builtin_amdgcn_sched_barrier(0);
+      wait_vm<(kStages - 3) * LPS>();
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      const int nxt = kt + kStages - 1;
+      char* st = smem + (nxt % kStages) * kStageBytes;
+      load_frags<NJ, T>(smem + ((kt + 1) % kStages) * kStageBytes, 0, rowbase, colbase, lr, lh,
+                        f0);
+      la.issue(st, (int64_t)nxt * BK, a.K);
+      issue_b(st + kTileBytes, (int64_t)nxt * BK);
       mfma_step<NJ, T>(f1, acc);
+#pragma unroll
+      for (int g = 0; g < kReadPairs; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
+      }
+#pragma unroll
+      for (int g = 0; g < LPS; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaHalf - kReadPairs - LPS, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     load_frags<NJ, T>(smem + ((nk - 1) % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
@@ -626,7 +651,7 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
   if (a.conv)
     hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kConvTileN, 3, 1, 0>), grid, dim3(256), 0, st, a);
   else
-    hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 4, 0, 1>), grid, dim3(512), 0, st, a);
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 4, 0, 2>), grid, dim3(512), 0, st, a);
 }
 
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {

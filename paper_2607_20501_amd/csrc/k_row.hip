@@ -136,7 +136,63 @@ hipError_t launch_row_wave_t(const RowArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Softmax finisher over the per-(row, column tile) partials (m_t, s_t) of a
+// GEMM epilogue: M = max_t m_t, S = sum_t s_t exp(m_t - M), then the row is
+// normalised in place, y = exp(c - M) / S.  One wave per row; lanes merge
+// the partials in parallel, and the row moves in 16-byte chunks, four in
+// flight per lane.
+template <typename T>
+__global__ __launch_bounds__(256) void softmax_finish_wave_kernel(const float* partial, int64_t rows,
+                                                                  int64_t nt, int64_t N, T* out) {
+  constexpr int E = kEpv<T>;
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;   // whole wave exits together
+  const float* pr = partial + r * nt * 2;
+  float m = -INFINITY;
+  for (int64_t t = lane; t < nt; t += 64) m = fmaxf(m, pr[t * 2]);
+  const float M = warp_max(m);
+  float s = 0.f;
+  for (int64_t t = lane; t < nt; t += 64) {
+    const float mt = pr[t * 2];
+    if (mt != -INFINITY) s += pr[t * 2 + 1] * __expf(mt - M);
+  }
+  const float inv = 1.0f / warp_sum(s);
+  T* y = out + r * N;
+  const int64_t chunks = N / E;
+  for (int64_t c0 = lane; c0 < chunks; c0 += 64 * 4) {
+    float v[4][E];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (c0 + u * 64 < chunks) ld_vec<T>(y + (c0 + u * 64) * E, v[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (c0 + u * 64 < chunks) {
+#pragma unroll
+        for (int k = 0; k < E; ++k) v[u][k] = __expf(v[u][k] - M) * inv;
+        st_vec<T>(y + (c0 + u * 64) * E, v[u]);
+      }
+  }
+}
+
 }  // namespace
+
+bool softmax_finish_wave_supported(int dtype, int64_t N, const void* out) {
+  const int E = dtype == MK_BF16 ? 8 : 4;
+  return N % E == 0 && (uintptr_t)out % 16 == 0;
+}
+
+hipError_t launch_softmax_finish_wave(int dtype, const float* partial, int64_t rows, int64_t nt,
+                                      int64_t N, void* out, hipStream_t st) {
+  const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+  if (dtype == MK_BF16)
+    hipLaunchKernelGGL(softmax_finish_wave_kernel<bf16>, grid, block, 0, st, partial, rows, nt, N,
+                       (bf16*)out);
+  else
+    hipLaunchKernelGGL(softmax_finish_wave_kernel<float>, grid, block, 0, st, partial, rows, nt, N,
+                       (float*)out);
+  return hipGetLastError();
+}
 
 bool row_wave_supported(int dtype, const RowArgs& a) {
   const int E = dtype == MK_BF16 ? 8 : 4;

@@ -392,6 +392,8 @@ __global__ __launch_bounds__(256) void softmax_finish_kernel(const float* partia
 hipError_t launch_softmax_finish(int dtype, const float* partial, int64_t rows, int64_t nt,
                                  int64_t N, void* out, hipStream_t st) {
   if (rows == 0) return hipSuccess;
+  if (softmax_finish_wave_supported(dtype, N, out))
+    return launch_softmax_finish_wave(dtype, partial, rows, nt, N, out, st);
   if (dtype == 1)
     hipLaunchKernelGGL(softmax_finish_kernel<bf16>, dim3((unsigned)rows), dim3(256), 0, st,
                        partial, nt, N, (bf16*)out);

@@ -100,6 +100,9 @@ hipError_t launch_attn_simple(int dtype, const AttnArgs& a, hipStream_t st);
 // Tuned element-wise kernel (k_ew.hip): 16-byte groups, 32-bit index
 // arithmetic; ew_fast_supported() states when it applies.
 bool ew_fast_supported(const EwArgs& a);
+bool softmax_finish_wave_supported(int dtype, int64_t N, const void* out);
+hipError_t launch_softmax_finish_wave(int dtype, const float* partial, int64_t rows, int64_t nt,
+                                      int64_t N, void* out, hipStream_t st);
 hipError_t launch_ew_fast(int dtype, const EwArgs& a, hipStream_t st);
 // Column tiles of the bf16 MFMA GEMM for plain GEMMs and for conv GEMMs; the
 // per-tile partial layouts of the terminal finishers follow them.

@@ -51,8 +51,10 @@ def gemm_module(M, N, K, layout, dtype="bf16", epi=(), std=0.5):
     return {"name": "gemm", "dtype": dtype, "inputs": inputs, "recipes": recipes, "ops": ops}
 
 
+# (K of 8, 32, 64 and 96 give 1, 1, 2 and 3 K slices: fewer than the ring's
+# leading slices)
 SHAPES = [(256, 256, 64), (513, 264, 136), (300, 520, 200), (1000, 1024, 1024), (64, 8, 8),
-          (777, 1536, 328)]
+          (777, 1536, 328), (128, 512, 32), (300, 512, 96)]
 
 
 @pytest.mark.parametrize("layout", [0, 1])
@@ -116,7 +118,7 @@ def test_split_and_fused_agree_with_their_own_references():
 
 
 F32_SHAPES = [(256, 256, 64), (513, 264, 132), (300, 520, 200), (128, 256, 256),
-              (1000, 1024, 1028), (64, 4, 4)]
+              (1000, 1024, 1028), (64, 4, 4), (256, 256, 16), (300, 512, 32)]
 
 
 @pytest.mark.parametrize("layout", [0, 1])
