@@ -33,6 +33,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 namespace {
 
 constexpr int BQ = 128, BKV = 64, kThreads = 256;
+constexpr int kXcds = 8;
 constexpr uint32_t kOob = 0x80000000u;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
@@ -81,8 +82,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   const int64_t S = a.S, H = a.H;
   const int64_t ld3 = 3 * H * DH;
   const int nqb = (int)((S + BQ - 1) / BQ);
-  const int64_t z = blockIdx.x / nqb;
-  const int qb = nqb - 1 - (int)(blockIdx.x % nqb);      // heaviest first
+  // The hardware deals workgroups round-robin over the 8 XCDs.  When the
+  // grid divides evenly, the query blocks of one (batch, head) are all sent
+  // to one XCD (heaviest first), so that head's K and V are fetched into one
+  // L2 instead of eight.
+  int64_t bid = blockIdx.x;
+  const int64_t total = (int64_t)gridDim.x;
+  if (total % kXcds == 0) bid = (bid % kXcds) * (total / kXcds) + bid / kXcds;
+  const int64_t z = bid / nqb;
+  const int qb = nqb - 1 - (int)(bid % nqb);              // heaviest first
   const int64_t b = z / H, h = z % H;
   const int64_t q0 = (int64_t)qb * BQ;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
