@@ -91,21 +91,28 @@ def measured_traffic(workload, kernel):
 
 
 def time_module(mod, ins, out, ws, steps, warmup):
+    """ms per step over `steps` back-to-back runs (after `warmup` untimed
+    ones), bracketed by device synchronisation; then the same number of runs
+    again with a HIP event pair around every launch (on the module's stream)
+    for per-launch durations.  The event records add a few microseconds per
+    launch, so they stay out of the timed region."""
     import torch
     for _ in range(warmup):
         mod.run(ins, out, ws)
     torch.cuda.synchronize()
-    per_run = mod.launches_per_run()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    mod.profile_begin(per_run * steps)
-    torch.cuda.synchronize()
     start.record()
     for _ in range(steps):
         mod.run(ins, out, ws)
     end.record()
     torch.cuda.synchronize()
-    launch_ms = mod.profile_end(per_run * steps)
     ms = start.elapsed_time(end) / steps
+    per_run = mod.launches_per_run()
+    mod.profile_begin(per_run * steps)
+    for _ in range(steps):
+        mod.run(ins, out, ws)
+    torch.cuda.synchronize()
+    launch_ms = mod.profile_end(per_run * steps)
     per_launch = [sum(launch_ms[k::per_run]) / steps for k in range(per_run)]
     return ms, per_launch
 
