@@ -3,8 +3,10 @@
 // Every family has a tuned implementation (MK_IMPL_TUNED) and a simple one
 // (MK_IMPL_SIMPLE); a subkernel's implementation can be swapped without
 // touching the others (MKEvolve Sec. 3, "Swap").  Ids >= 100 are test-only
-// mutants reproducing the injected bugs of App. D, used to show that
-// per-stage verification catches them.
+// mutants reproducing the eleven injected bugs of App. D (five attention,
+// six FFN; the tile-boundary and accumulator bugs serve both blocks), used to
+// show that per-stage verification catches them.  Mutants run on the simple
+// kernels, except the epilogue-chain ones, which rewrite the chain.
 #include "impls.hpp"
 
 #include <algorithm>
@@ -15,11 +17,15 @@
 namespace mk {
 
 enum Mutant : int32_t {
-  MUT_MASK_OFF_BY_ONE = 102,  // the diagonal is masked too
-  MUT_TILE_BOUNDARY = 103,    // the last K slice of the contraction is not loaded
-  MUT_GELU_SIGMOID = 107,     // x * sigmoid(1.702 x) instead of exact GELU
-  MUT_NO_RESIDUAL = 108,      // residual add dropped
-  MUT_RELU_FOR_GELU = 109     // ReLU instead of GELU
+  MUT_UNSAFE_SOFTMAX = 101,     // exp(x) without the row max subtracted
+  MUT_MASK_OFF_BY_ONE = 102,    // the diagonal is masked too
+  MUT_TILE_BOUNDARY = 103,      // the last partial (or last 16-deep) K tile is not loaded
+  MUT_BF16_ACCUM = 104,         // the contraction accumulates in bf16
+  MUT_SOFTMAX_WRONG_DIM = 105,  // softmax over dim -2 instead of -1
+  MUT_UNSAFE_LAYERNORM = 106,   // rows scaled by 1/sigma without subtracting the mean
+  MUT_GELU_SIGMOID = 107,       // x * sigmoid(1.702 x) instead of exact GELU
+  MUT_NO_RESIDUAL = 108,        // residual add dropped
+  MUT_RELU_FOR_GELU = 109       // ReLU instead of GELU
 };
 
 static bool chain_has(const EpiChain& c, int code) {
@@ -54,7 +60,17 @@ bool impl_exists(const Plan& p, const Subkernel& sk, int impl) {
     case MUT_MASK_OFF_BY_ONE:
       return (c && chain_has(*c, EPI_CAUSAL)) || (sk.family == MK_FAM_ATTN && sk.attn.causal);
     case MUT_TILE_BOUNDARY:
-      return sk.family == MK_FAM_GEMM && sk.gemm.K > 16;
+      return (sk.family == MK_FAM_GEMM && sk.gemm.K > 16) ||
+             (sk.family == MK_FAM_ATTN && sk.attn.dh > 16 && sk.attn.S * 4 <= 65536);
+    case MUT_UNSAFE_SOFTMAX:
+      return sk.family == MK_FAM_ROW && sk.row.op == MK_OP_SOFTMAX;
+    case MUT_SOFTMAX_WRONG_DIM:
+      return sk.family == MK_FAM_ROW && sk.row.op == MK_OP_SOFTMAX && sk.row.n2 > 1;
+    case MUT_BF16_ACCUM:
+      return sk.family == MK_FAM_GEMM;
+    case MUT_UNSAFE_LAYERNORM:
+      return (sk.family == MK_FAM_ROW && sk.row.op == MK_OP_LAYERNORM) ||
+             (sk.family == MK_FAM_GEMM && sk.gemm.ln);
     case MUT_GELU_SIGMOID: case MUT_RELU_FOR_GELU:
       return c && chain_has_gelu(*c);
     case MUT_NO_RESIDUAL:
@@ -220,6 +236,11 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       a.beta = r.b_value >= 0 ? vals[r.b_value] : nullptr;
       a.eps = r.eps;
       a.pre = ew_args(r.pre, vals, nullptr, impl);
+      a.n2 = r.n2;
+      a.variant = impl == MUT_UNSAFE_SOFTMAX      ? 1
+                  : impl == MUT_SOFTMAX_WRONG_DIM ? 2
+                  : impl == MUT_UNSAFE_LAYERNORM  ? 3
+                                                  : 0;
       return hip_check(timed([&] { return launch_row(dt, a, st, impl); }), "row");
     }
     case MK_FAM_GEMM: {
@@ -238,6 +259,7 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       a.layout = g.layout;
       a.terminal = g.terminal;
       a.alpha = g.alpha;
+      a.acc_bf16 = impl == MUT_BF16_ACCUM ? 1 : 0;
       a.epi = resolve(g.epi, vals, impl);
       if (impl == MUT_TILE_BOUNDARY) a.K = g.K - ((g.K % 16) ? (g.K % 16) : 16);
       const GemmScratch gs = gemm_scratch(p, sk, impl);
@@ -264,7 +286,8 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
           float* stats = (float*)sc;
           mk_status s = hip_check(timed([&] {
                                     return launch_ln_stats(dt, vals[g.a_value], g.M, g.K, g.eps,
-                                                           stats, st);
+                                                           stats, st,
+                                                           impl == MUT_UNSAFE_LAYERNORM);
                                   }),
                                   "layernorm stats");
           if (s != MK_OK) return s;
@@ -335,7 +358,9 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       a.B = t.B; a.H = t.H; a.dh = t.dh; a.S = t.S;
       a.scale = t.scale;
       a.causal = t.causal ? (impl == MUT_MASK_OFF_BY_ONE ? 2 : 1) : 0;
-      const bool fused = impl != MK_IMPL_SIMPLE && attn_fused_supported(dt, a) &&
+      a.kdim = impl == MUT_TILE_BOUNDARY ? t.dh - ((t.dh % 16) ? (t.dh % 16) : 16) : t.dh;
+      const bool fused = impl != MK_IMPL_SIMPLE && impl != MUT_TILE_BOUNDARY &&
+                         attn_fused_supported(dt, a) &&
                          (uintptr_t)a.qkv % 16 == 0 && (uintptr_t)a.o % 16 == 0;
       return hip_check(timed([&] {
                          return fused ? launch_attn_fused(dt, a, st)

@@ -149,6 +149,7 @@ __global__ __launch_bounds__(256) void row_kernel(RowArgs a) {
       float m = -INFINITY;
       for (int64_t j = threadIdx.x; j < L; j += blockDim.x) m = fmaxf(m, row_in<T>(a, r, j));
       m = block_max(m, red);
+      if (a.variant == 1) m = 0.f;   // test-only: the max is not subtracted
       float s = 0.f;
       for (int64_t j = threadIdx.x; j < L; j += blockDim.x) s += __expf(row_in<T>(a, r, j) - m);
       s = block_sum(s, red);
@@ -167,8 +168,9 @@ __global__ __launch_bounds__(256) void row_kernel(RowArgs a) {
         q += d * d;
       }
       const float rstd = rsqrtf(block_sum(q, red) / (float)L + a.eps);
+      const float shift = a.variant == 3 ? 0.f : mu;   // test-only: no centring
       for (int64_t j = threadIdx.x; j < L; j += blockDim.x) {
-        const float v = (row_in<T>(a, r, j) - mu) * rstd * ld<T>((const T*)a.gamma, j) +
+        const float v = (row_in<T>(a, r, j) - shift) * rstd * ld<T>((const T*)a.gamma, j) +
                         ld<T>((const T*)a.beta, j);
         st<T>((T*)a.y, r * L + j, v);
       }
@@ -179,9 +181,35 @@ __global__ __launch_bounds__(256) void row_kernel(RowArgs a) {
   }
 }
 
+// Test-only: softmax over dim -2, i.e. down each column of every group of n2
+// consecutive rows.  One thread per column.
+template <typename T>
+__global__ void softmax_col_kernel(RowArgs a) {
+  const int64_t L = a.len, groups = a.rows / a.n2;
+  const int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (c >= groups * L) return;
+  const int64_t g = c / L, j = c % L, r0 = g * a.n2;
+  float m = -INFINITY;
+  for (int64_t i = 0; i < a.n2; ++i) m = fmaxf(m, row_in<T>(a, r0 + i, j));
+  float s = 0.f;
+  for (int64_t i = 0; i < a.n2; ++i) s += __expf(row_in<T>(a, r0 + i, j) - m);
+  for (int64_t i = 0; i < a.n2; ++i)
+    st<T>((T*)a.y, (r0 + i) * L + j, __expf(row_in<T>(a, r0 + i, j) - m) / s);
+}
+
 hipError_t launch_row(int dtype, const RowArgs& a, hipStream_t st, int impl) {
   if (a.rows == 0) return hipSuccess;
-  if (impl != MK_IMPL_SIMPLE && row_wave_supported(dtype, a)) return launch_row_wave(dtype, a, st);
+  if (a.variant == 2) {
+    if (a.op != MK_OP_SOFTMAX || a.n2 < 1 || a.rows % a.n2) return hipErrorInvalidValue;
+    const unsigned g = (unsigned)((a.rows / a.n2 * a.len + 255) / 256);
+    if (dtype == 1)
+      hipLaunchKernelGGL(softmax_col_kernel<bf16>, dim3(g), dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL(softmax_col_kernel<float>, dim3(g), dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
+  if (a.variant == 0 && impl != MK_IMPL_SIMPLE && row_wave_supported(dtype, a))
+    return launch_row_wave(dtype, a, st);
   if (dtype == 1)
     hipLaunchKernelGGL(row_kernel<bf16>, dim3((unsigned)a.rows), dim3(256), 0, st, a);
   else
@@ -192,7 +220,7 @@ hipError_t launch_row(int dtype, const RowArgs& a, hipStream_t st, int impl) {
 // Per-row (mean, rstd) for a LayerNorm applied as a GEMM prologue.
 template <typename T>
 __global__ __launch_bounds__(256) void ln_stats_kernel(const T* x, int64_t len, float eps,
-                                                       float* stats) {
+                                                       float* stats, int unsafe) {
   __shared__ float red[16];
   const int64_t r = blockIdx.x;
   const T* xr = x + r * len;
@@ -206,20 +234,20 @@ __global__ __launch_bounds__(256) void ln_stats_kernel(const T* x, int64_t len, 
   }
   const float var = block_sum(q, red) / (float)len;
   if (threadIdx.x == 0) {
-    stats[2 * r] = mu;
+    stats[2 * r] = unsafe ? 0.f : mu;   // test-only: no centring
     stats[2 * r + 1] = rsqrtf(var + eps);
   }
 }
 
 hipError_t launch_ln_stats(int dtype, const void* x, int64_t rows, int64_t len, float eps,
-                           float* stats, hipStream_t st) {
+                           float* stats, hipStream_t st, int unsafe) {
   if (rows == 0) return hipSuccess;
   if (dtype == 1)
     hipLaunchKernelGGL(ln_stats_kernel<bf16>, dim3((unsigned)rows), dim3(256), 0, st,
-                       (const bf16*)x, len, eps, stats);
+                       (const bf16*)x, len, eps, stats, unsafe);
   else
     hipLaunchKernelGGL(ln_stats_kernel<float>, dim3((unsigned)rows), dim3(256), 0, st,
-                       (const float*)x, len, eps, stats);
+                       (const float*)x, len, eps, stats, unsafe);
   return hipGetLastError();
 }
 
@@ -283,10 +311,17 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmArgs a) {
       for (int i = 0; i < 4; ++i) ar[i] = As[kk][ty * 4 + i];
 #pragma unroll
       for (int j = 0; j < 4; ++j) br[j] = Bs[kk][tx * 4 + j];
+      if (a.acc_bf16) {   // test-only: a bf16 accumulator
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(ar[i], br[j], acc[i][j]);
+          for (int j = 0; j < 4; ++j) acc[i][j] = rnd<bf16>(fmaf(ar[i], br[j], acc[i][j]));
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(ar[i], br[j], acc[i][j]);
+      }
     }
     __syncthreads();
   }
@@ -487,7 +522,7 @@ __global__ __launch_bounds__(256) void attn_simple_kernel(AttnArgs a) {
   for (int64_t j = threadIdx.x; j < jmax; j += blockDim.x) {
     const T* k = qkv + (b * a.S + j) * ld3 + a.H * a.dh + h * a.dh;
     float s = 0.f;
-    for (int64_t e = 0; e < a.dh; ++e) s = fmaf(ld<T>(q, e), ld<T>(k, e), s);
+    for (int64_t e = 0; e < a.kdim; ++e) s = fmaf(ld<T>(q, e), ld<T>(k, e), s);
     s *= a.scale;
     sc[j] = s;
     m = fmaxf(m, s);

@@ -34,6 +34,11 @@ struct RowArgs {
   const void* beta;
   float eps;
   EwArgs pre;              // element-wise prologue (pre.epi.n == 0: none)
+  // Test-only variants (simple kernel): 1 softmax without the max
+  // subtracted, 2 softmax over dim -2 (n2 rows of each group of rows),
+  // 3 LayerNorm without the mean subtracted before scaling.
+  int32_t variant;
+  int64_t n2;
 };
 
 struct GemmArgs {
@@ -44,6 +49,7 @@ struct GemmArgs {
   int64_t a_off, a_sb, a_sh, b_off, b_sb, b_sh, c_off, c_sb, c_sh;
   int32_t batch, heads, layout, terminal;
   float alpha;
+  int32_t acc_bf16;        // test-only: round the accumulator to bf16 after every step
   const float* ln_stats;   // [M][2] (mean, rstd) of A's rows, or null
   const void* ln_g;
   const void* ln_b;
@@ -77,6 +83,7 @@ struct AttnArgs {
   int64_t B, H, dh, S;
   float scale;
   int32_t causal;
+  int64_t kdim;            // dims of q.k summed (dh; test-only: fewer)
 };
 
 // dtype: 0 float32, 1 bfloat16 (mk_dtype).
@@ -86,8 +93,9 @@ hipError_t launch_row(int dtype, const RowArgs& a, hipStream_t st, int impl);
 // 8 bf16 / 4 fp32 elements, at most 4096 / 2048, 16-byte aligned buffers).
 bool row_wave_supported(int dtype, const RowArgs& a);
 hipError_t launch_row_wave(int dtype, const RowArgs& a, hipStream_t st);
+// unsafe (test-only): the mean is reported as 0, so rows are not centred.
 hipError_t launch_ln_stats(int dtype, const void* x, int64_t rows, int64_t len, float eps,
-                           float* stats, hipStream_t st);
+                           float* stats, hipStream_t st, int unsafe);
 hipError_t launch_gemm_simple(int dtype, const GemmArgs& a, hipStream_t st);
 hipError_t launch_rowsum_finish(int dtype, const float* partial, int64_t rows, int64_t n_tiles,
                                 void* out, hipStream_t st);

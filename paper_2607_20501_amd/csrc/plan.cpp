@@ -423,6 +423,7 @@ bool match_group(const Plan& p, int32_t b, int32_t e, Subkernel& sk, std::string
       } else {
         r.len = xin.dims[xin.ndim - 1];
         r.rows = numel(xin) / r.len;
+        r.n2 = xin.ndim >= 2 ? xin.dims[xin.ndim - 2] : 1;
       }
       if (last.kind == MK_OP_LAYERNORM) {
         r.g_value = last.in[1];

@@ -75,6 +75,7 @@ struct RowSpec {
   EwSpec pre;                  // element-wise prologue on the input (indexing as EwSpec)
   int32_t g_value = -1, b_value = -1;
   float eps = 0.f;
+  int64_t n2 = 1;              // size of the input's dim -2 (1 for a vector)
 };
 
 struct AttnSpec {

@@ -106,6 +106,29 @@ def transformer_layer(B=8, S=2048, D=2048, H=16, F=8192, dtype="bf16", eps=1e-5,
     }
 
 
+def causal_attention_block(B=2, S=256, D=512, H=4, dtype="bf16", x_std=1.0):
+    """MinGPT-style causal self-attention without residual (App. D case 1):
+    QKV projection -> scaled q.k -> causal mask -> softmax -> PV -> output
+    projection.  x ~ N(0, x_std); W ~ N(0, 0.02)."""
+    dh = D // H
+    w = (NORMAL, 0.0, 0.02)
+    n = 3
+    return {
+        "name": f"causal_attention_b{B}_s{S}_d{D}_h{H}_{dtype}",
+        "dtype": dtype,
+        "inputs": [[B, S, D], [3 * D, D], [D, D]],
+        "recipes": [(NORMAL, 0.0, x_std), w, w],
+        "ops": [
+            _op("GEMM", [0, 1], [0]),                                  # 0 qkv
+            _op("QK", [n + 0], [B, H, dh, S], [1.0 / math.sqrt(dh)]),  # 1
+            _op("CAUSAL_MASK", [n + 1]),                               # 2
+            _op("SOFTMAX", [n + 2]),                                   # 3
+            _op("PV", [n + 3, n + 0], [B, H, dh, S]),                  # 4
+            _op("GEMM", [n + 4, 2], [0]),                              # 5 out-proj
+        ],
+    }
+
+
 def full_size(k):
     """The five full-size workloads, numbered as in the benchmark's config list
     (1-based): 1 linear+ReLU+row-sum fp32, 2 GEMM+GELU+softmax bf16,
