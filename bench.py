@@ -250,6 +250,13 @@ def main():
     sk = fused.subkernels()
     launch_to_sub = [i for i, s in enumerate(sk) for _ in range(s["n_launches"])]
     sub = sk[launch_to_sub[k]]
+    sub_ms = [0.0] * len(sk)
+    for i, t in enumerate(per_launch):
+        sub_ms[launch_to_sub[i]] += t
+    result["subkernel_us"] = [round(t * 1e3, 2) for t in sub_ms]
+    # runtime attribution of the composition (the share a budget allocation by
+    # runtime would give each subkernel)
+    result["subkernel_share"] = [round(x, 4) for x in mk.mk_budget_shares(sub_ms)]
     bf = module["dtype"] == "bf16"
     if sub["flops"] > 0:
         achieved = sub["flops"] / (per_launch[k] * 1e-3) / 1e12

@@ -220,6 +220,39 @@ mk_status mk_verify(mk_module* m, const void* const* dev_inputs, void* dev_out, 
                     int64_t ws_bytes, void* stream, int32_t n_checks, const mk_check* checks,
                     mk_verify_report* report);
 
+/* Swap policy (Sec. 3, "Swap"; Alg. 1): subkernel i's speedup is
+ * ms_reference[i] / ms_selected[i], the time of the reference implementation
+ * over the time of the selected one.  When there are at least two subkernels
+ * and at least one of them is not slower than its reference (speedup >= 1),
+ * every subkernel with speedup < tau is marked for replacement by the
+ * reference (swap[i] = 1); otherwise nothing is (*triggered = 0).  A
+ * subkernel with no reference time (ms_reference[i] < 0) is never swapped.
+ * Pure host function: arrays are host memory of length n, swap is written,
+ * triggered may be NULL.  MK_E_INVALID_ARG on a null array or n < 0. */
+mk_status mk_swap_decide(int32_t n, const float* ms_selected, const float* ms_reference,
+                         float tau, int32_t* swap, int32_t* triggered);
+
+/* The swap policy applied to a module: every subkernel is timed with its
+ * selected implementation and with reference_impl (usually MK_IMPL_SIMPLE),
+ * n_runs runs each after one warm-up run (mean of the HIP-event times of
+ * mk_run, which synchronises), then mk_swap_decide runs and the marked
+ * subkernels are switched to reference_impl.  Subkernels without
+ * reference_impl keep their implementation.  Buffers as for mk_run; the
+ * output buffer holds the last run's result.  The optional host arrays
+ * [n_subkernels] receive the times and the decision. */
+mk_status mk_swap(mk_module* m, const void* const* dev_inputs, void* dev_out, void* dev_ws,
+                  int64_t ws_bytes, void* stream, int32_t reference_impl, float tau,
+                  int32_t n_runs, float* ms_selected, float* ms_reference, int32_t* swapped,
+                  int32_t* triggered);
+
+/* Budget allocation over subkernels (the AllocateLLMBudget rule of Sec. 3):
+ * if any subkernel has needs_work[i] != 0 (new or failing verification), the
+ * budget is shared evenly among those; otherwise in proportion to ms[i] (the
+ * last end-to-end run's per-subkernel time).  shares[n] sums to 1 (all 0 if
+ * every ms is 0).  Pure host function; needs_work may be NULL. */
+mk_status mk_budget_shares(int32_t n, const float* ms, const int32_t* needs_work,
+                           float* shares);
+
 const char* mk_status_str(mk_status s);
 const char* mk_last_error(void);
 

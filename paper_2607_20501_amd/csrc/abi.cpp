@@ -224,6 +224,98 @@ mk_status mk_run(mk_module* m, const void* const* dev_inputs, void* dev_out, voi
   }
 }
 
+mk_status mk_swap_decide(int32_t n, const float* ms_selected, const float* ms_reference,
+                         float tau, int32_t* swap, int32_t* triggered) {
+  if (n < 0 || (n > 0 && (!ms_selected || !ms_reference || !swap)))
+    return fail(MK_E_INVALID_ARG, "mk_swap_decide: null array or n < 0");
+  bool any_fast = false;
+  for (int32_t i = 0; i < n; ++i) {
+    swap[i] = 0;
+    if (ms_reference[i] >= 0.f && ms_selected[i] > 0.f && ms_reference[i] >= ms_selected[i])
+      any_fast = true;
+  }
+  const bool go = n >= 2 && any_fast;
+  if (triggered) *triggered = go ? 1 : 0;
+  if (!go) return MK_OK;
+  for (int32_t i = 0; i < n; ++i) {
+    if (ms_reference[i] < 0.f || ms_selected[i] <= 0.f) continue;
+    swap[i] = ms_reference[i] / ms_selected[i] < tau ? 1 : 0;
+  }
+  return MK_OK;
+}
+
+mk_status mk_budget_shares(int32_t n, const float* ms, const int32_t* needs_work,
+                           float* shares) {
+  if (n < 0 || (n > 0 && (!ms || !shares)))
+    return fail(MK_E_INVALID_ARG, "mk_budget_shares: null array or n < 0");
+  int32_t n_work = 0;
+  double total = 0.0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (needs_work && needs_work[i]) ++n_work;
+    if (ms[i] < 0.f) return fail(MK_E_INVALID_ARG, "mk_budget_shares: negative time");
+    total += ms[i];
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    if (n_work)
+      shares[i] = needs_work[i] ? 1.0f / (float)n_work : 0.f;
+    else
+      shares[i] = total > 0.0 ? (float)(ms[i] / total) : 0.f;
+  }
+  return MK_OK;
+}
+
+mk_status mk_swap(mk_module* m, const void* const* dev_inputs, void* dev_out, void* dev_ws,
+                  int64_t ws_bytes, void* stream, int32_t reference_impl, float tau,
+                  int32_t n_runs, float* ms_selected, float* ms_reference, int32_t* swapped,
+                  int32_t* triggered) {
+  if (!m || n_runs < 1) return fail(MK_E_INVALID_ARG, "null module or n_runs < 1");
+  try {
+    mk::Plan& p = m->plan;
+    const size_t ns = p.subs.size();
+    std::vector<int32_t> sel(ns), has_ref(ns);
+    for (size_t i = 0; i < ns; ++i) {
+      sel[i] = p.subs[i].impl;
+      has_ref[i] = mk::impl_exists(p, p.subs[i], reference_impl) ? 1 : 0;
+    }
+    // mean per-subkernel time over n_runs runs (after one warm-up)
+    auto time_all = [&](std::vector<float>& mean) -> mk_status {
+      std::vector<float> t(ns);
+      mean.assign(ns, 0.f);
+      for (int32_t r = 0; r <= n_runs; ++r) {
+        mk_status s = mk_run(m, dev_inputs, dev_out, dev_ws, ws_bytes, stream, t.data());
+        if (s != MK_OK) return s;
+        if (r > 0)
+          for (size_t i = 0; i < ns; ++i) mean[i] += t[i] / (float)n_runs;
+      }
+      return MK_OK;
+    };
+    std::vector<float> t_sel, t_ref;
+    mk_status s = time_all(t_sel);
+    if (s != MK_OK) return s;
+    for (size_t i = 0; i < ns; ++i)
+      if (has_ref[i]) p.subs[i].impl = reference_impl;
+    s = time_all(t_ref);
+    for (size_t i = 0; i < ns; ++i) p.subs[i].impl = sel[i];
+    if (s != MK_OK) return s;
+    for (size_t i = 0; i < ns; ++i)
+      if (!has_ref[i]) t_ref[i] = -1.f;
+    std::vector<int32_t> sw(ns);
+    int32_t trig = 0;
+    s = mk_swap_decide((int32_t)ns, t_sel.data(), t_ref.data(), tau, sw.data(), &trig);
+    if (s != MK_OK) return s;
+    for (size_t i = 0; i < ns; ++i) {
+      if (sw[i]) p.subs[i].impl = reference_impl;
+      if (ms_selected) ms_selected[i] = t_sel[i];
+      if (ms_reference) ms_reference[i] = t_ref[i];
+      if (swapped) swapped[i] = sw[i];
+    }
+    if (triggered) *triggered = trig;
+    return MK_OK;
+  } catch (...) {
+    return fail(MK_E_INTERNAL, "exception in mk_swap");
+  }
+}
+
 mk_status mk_profile_begin(mk_module* m, int32_t max_launches) {
   if (!m || max_launches < 1) return fail(MK_E_INVALID_ARG, "null module or max_launches < 1");
   if (m->profiling) return fail(MK_E_INVALID_ARG, "a profile is already open");

@@ -82,7 +82,8 @@ class mk_verify_report(ctypes.Structure):
 
 EXPORTS = ["mk_decomposition_preset", "mk_module_create", "mk_module_destroy", "mk_module_info",
            "mk_subkernel_info", "mk_subkernel_select", "mk_workspace_size", "mk_run",
-           "mk_verify", "mk_status_str", "mk_last_error", "mk_profile_begin", "mk_profile_end"]
+           "mk_verify", "mk_status_str", "mk_last_error", "mk_profile_begin", "mk_profile_end",
+           "mk_swap_decide", "mk_swap", "mk_budget_shares"]
 
 _lib = None
 
@@ -116,6 +117,13 @@ def load():
     lib.mk_profile_end.argtypes = [vp, P(ctypes.c_float), ctypes.c_int32, P(ctypes.c_int32)]
     lib.mk_profile_begin.restype = ctypes.c_int
     lib.mk_profile_end.restype = ctypes.c_int
+    fp, ip = P(ctypes.c_float), P(ctypes.c_int32)
+    lib.mk_swap_decide.argtypes = [ctypes.c_int32, fp, fp, ctypes.c_float, ip, ip]
+    lib.mk_swap.argtypes = [vp, P(vp), vp, vp, ctypes.c_int64, vp, ctypes.c_int32,
+                            ctypes.c_float, ctypes.c_int32, fp, fp, ip, ip]
+    lib.mk_budget_shares.argtypes = [ctypes.c_int32, fp, ip, fp]
+    for f in ("mk_swap_decide", "mk_swap", "mk_budget_shares"):
+        getattr(lib, f).restype = ctypes.c_int
     lib.mk_status_str.argtypes = [ctypes.c_int]
     lib.mk_status_str.restype = ctypes.c_char_p
     lib.mk_last_error.argtypes = []
@@ -263,6 +271,26 @@ def mk_verify(h, dev_inputs, dev_out, dev_ws, ws_bytes, stream, checks):
             "results": res}
 
 
+def mk_swap_decide(ms_selected, ms_reference, tau):
+    """-> (swap flags, triggered) for per-subkernel times (host lists)."""
+    n = len(ms_selected)
+    a = (ctypes.c_float * max(1, n))(*ms_selected)
+    b = (ctypes.c_float * max(1, n))(*ms_reference)
+    sw = (ctypes.c_int32 * max(1, n))()
+    trig = ctypes.c_int32()
+    _check(load().mk_swap_decide(n, a, b, float(tau), sw, ctypes.byref(trig)))
+    return [int(x) for x in sw[:n]], bool(trig.value)
+
+
+def mk_budget_shares(ms, needs_work=None):
+    n = len(ms)
+    a = (ctypes.c_float * max(1, n))(*ms)
+    w = (ctypes.c_int32 * max(1, n))(*(needs_work or [0] * n)) if needs_work is not None else None
+    out = (ctypes.c_float * max(1, n))()
+    _check(load().mk_budget_shares(n, a, w, out))
+    return list(out[:n])
+
+
 # ------------------------------------------------------------------ convenience
 
 class Module:
@@ -311,6 +339,23 @@ class Module:
                       ws.data_ptr() if ws is not None and ws.numel() else None,
                       ws.numel() * ws.element_size() if ws is not None else 0, st,
                       self.n if timing else None)
+
+    def swap(self, dev_inputs, out, ws, reference_impl=IMPL_SIMPLE, tau=0.9, n_runs=5,
+             stream=None):
+        """Apply the swap policy (mk_swap); returns the per-subkernel times and
+        decision."""
+        st = stream.cuda_stream if stream is not None else _current_stream()
+        n = self.n
+        t_sel, t_ref = (ctypes.c_float * n)(), (ctypes.c_float * n)()
+        sw, trig = (ctypes.c_int32 * n)(), ctypes.c_int32()
+        ptrs = (ctypes.c_void_p * max(1, len(dev_inputs)))(*self._ptrs(dev_inputs))
+        _check(load().mk_swap(self.h, ptrs, out.data_ptr(),
+                              ws.data_ptr() if ws is not None and ws.numel() else None,
+                              ws.numel() * ws.element_size() if ws is not None else 0, st,
+                              int(reference_impl), float(tau), int(n_runs), t_sel, t_ref, sw,
+                              ctypes.byref(trig)))
+        return {"ms_selected": list(t_sel), "ms_reference": list(t_ref),
+                "swapped": [int(x) for x in sw], "triggered": bool(trig.value)}
 
     def verify(self, dev_inputs, out, ws, checks, stream=None):
         st = stream.cuda_stream if stream is not None else _current_stream()
