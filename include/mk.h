@@ -71,11 +71,16 @@ typedef enum { MK_F32 = 0, MK_BF16 = 1 } mk_dtype;
  *               fp[0] = scale: s[b,h,i,j] = (q_i . k_j) * scale -> [B,H,S,S].
  *  CAUSAL_MASK  [..,S,S]: entries with j > i become -inf (diagonal kept).
  *  PV           in {p[B,H,S,S], qkv}, ip = {B, H, dh, S}:
- *               o[b,i,h*dh+e] = sum_j p[b,h,i,j] v[b,j,h,e] -> [B,S,H*dh]. */
+ *               o[b,i,h*dh+e] = sum_j p[b,h,i,j] v[b,j,h,e] -> [B,S,H*dh].
+ *  GMP          [N,C,H,W] -> [N,C]: max over H*W (global max pool).
+ *  LPPOOL       [N,C,H,W] -> [N,C], fp[0] = p > 0: S = sum over H*W of x^p,
+ *               y = sign(S) |S|^(1/p) (global LP pool; the pooling variants
+ *               that replace GAP in Sec. 4's MobileNet adaptation). */
 typedef enum {
   MK_OP_GEMM = 0, MK_OP_BIAS, MK_OP_BIAS_CHANNEL, MK_OP_RELU, MK_OP_GELU_ERF,
   MK_OP_GELU_TANH, MK_OP_SCALE, MK_OP_ADD, MK_OP_ROWSUM, MK_OP_SOFTMAX,
   MK_OP_LAYERNORM, MK_OP_CONV2D, MK_OP_GAP, MK_OP_QK, MK_OP_CAUSAL_MASK, MK_OP_PV,
+  MK_OP_GMP, MK_OP_LPPOOL,
   MK_OP_COUNT
 } mk_op_kind;
 

@@ -160,8 +160,9 @@ static int infer_shapes(const mko_desc* d, mko_shape* vs) {
         y.dims[3] = wp / st + 1;
         break;
       }
-      case MKO_GAP:
+      case MKO_GAP: case MKO_GMP: case MKO_LPPOOL:
         if (x->ndim != 4) return -2;
+        if (o->kind == MKO_LPPOOL && !(o->fp[0] > 0.0)) return -2;
         y.ndim = 2;
         break;
       case MKO_QK: case MKO_PV: {
@@ -562,6 +563,25 @@ int mko_run(const mko_desc* d, const int32_t* group_of_op, const void* const* ho
           double s = 0.0;
           for (int64_t k = 0; k < hw; ++k) s += x[r * hw + k];
           y[r] = s / (double)hw;
+        }
+        break;
+      }
+      case MKO_GMP: {   /* global max pool (a MobileNet-style pooling variant, Sec. 4) */
+        int64_t hw = xs->dims[2] * xs->dims[3];
+        for (int64_t r = 0; r < n; ++r) {
+          double m = -INFINITY;
+          for (int64_t k = 0; k < hw; ++k) m = x[r * hw + k] > m ? x[r * hw + k] : m;
+          y[r] = m;
+        }
+        break;
+      }
+      case MKO_LPPOOL: {   /* global LP pool: (sum x^p)^(1/p), sign kept */
+        int64_t hw = xs->dims[2] * xs->dims[3];
+        double p = o->fp[0];
+        for (int64_t r = 0; r < n; ++r) {
+          double s = 0.0;
+          for (int64_t k = 0; k < hw; ++k) s += pow(x[r * hw + k], p);
+          y[r] = copysign(pow(fabs(s), 1.0 / p), s);
         }
         break;
       }

@@ -40,6 +40,9 @@ enum mko_kind {
   MKO_QK,            /* in {qkv[B*S, 3*H*dh]}; ip={B,H,dh,S}; fp[0]=scale -> [B,H,S,S] */
   MKO_CAUSAL_MASK,   /* [.., S, S]: j > i -> -inf, diagonal kept */
   MKO_PV,            /* in {p[B,H,S,S], qkv}; ip={B,H,dh,S} -> [B,S,H*dh] */
+  MKO_GMP,           /* [N,C,H,W] -> [N,C], max over H*W */
+  MKO_LPPOOL,        /* [N,C,H,W] -> [N,C], fp[0] = p: S = sum x^p over H*W,
+                        y = sign(S) |S|^(1/p) */
   MKO_N_KINDS
 };
 

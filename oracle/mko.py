@@ -15,7 +15,8 @@ _LIB = os.path.join(_HERE, "libmko.so")
 _lib = None
 
 KINDS = ["GEMM", "BIAS", "BIAS_CHANNEL", "RELU", "GELU_ERF", "GELU_TANH", "SCALE", "ADD",
-         "ROWSUM", "SOFTMAX", "LAYERNORM", "CONV2D", "GAP", "QK", "CAUSAL_MASK", "PV"]
+         "ROWSUM", "SOFTMAX", "LAYERNORM", "CONV2D", "GAP", "QK", "CAUSAL_MASK", "PV",
+         "GMP", "LPPOOL"]
 MAX_OPS = 64
 
 

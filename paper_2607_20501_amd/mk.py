@@ -13,7 +13,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmk.so")
 
 KINDS = ["GEMM", "BIAS", "BIAS_CHANNEL", "RELU", "GELU_ERF", "GELU_TANH", "SCALE", "ADD",
-         "ROWSUM", "SOFTMAX", "LAYERNORM", "CONV2D", "GAP", "QK", "CAUSAL_MASK", "PV"]
+         "ROWSUM", "SOFTMAX", "LAYERNORM", "CONV2D", "GAP", "QK", "CAUSAL_MASK", "PV",
+         "GMP", "LPPOOL"]
 FAMILIES = ["GEMM", "CONV", "EW", "ROW", "ATTN"]
 STATUS = ["MK_OK", "MK_E_INVALID_ARG", "MK_E_SHAPE", "MK_E_DTYPE", "MK_E_DECOMP",
           "MK_E_UNSUPPORTED", "MK_E_WORKSPACE", "MK_E_HIP", "MK_E_INTERNAL"]

@@ -198,6 +198,40 @@ def test_rowsum_and_gap():
         run1(module("f32", [(1, 2, 3, 3)], [op("GAP", [0])]), f32_inputs(c))[0], [[2.5, 2.5]])
 
 
+def test_global_max_and_lp_pool():
+    """GMP and LPPOOL (pooling variants of Sec. 4): hand values, the torch CPU
+    pooling routines in float64, and p = 1 / p = 2 special cases."""
+    x = np.array([[[[1.0, -2.0], [5.0, 0.5]], [[-3.0, -1.0], [-7.0, -2.0]]]])   # [1,2,2,2]
+    m = module("f32", [x.shape], [op("GMP", [0])])
+    assert run1(m, f32_inputs(x))[-1].tolist() == [[5.0, -1.0]]
+    m = module("f32", [x.shape], [op("LPPOOL", [0], fp=[2.0])])
+    np.testing.assert_allclose(run1(m, f32_inputs(x))[-1],
+                               [[math.sqrt(1 + 4 + 25 + 0.25), math.sqrt(9 + 1 + 49 + 4)]],
+                               rtol=1e-15)
+    # odd p keeps the sign of the sum: channel 1 sums to -(27 + 1 + 343 + 8)
+    m = module("f32", [x.shape], [op("LPPOOL", [0], fp=[3.0])])
+    got = run1(m, f32_inputs(x))[-1]
+    np.testing.assert_allclose(got[0, 1], -(379.0 ** (1 / 3)), rtol=1e-14)
+    np.testing.assert_allclose(got[0, 0], (1 - 8 + 125 + 0.125) ** (1 / 3), rtol=1e-14)
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((3, 4, 6, 5)).astype(np.float32)
+    xt = torch.from_numpy(x.astype(np.float64))
+    m = module("f32", [x.shape], [op("GMP", [0])])
+    ref = torch.nn.functional.max_pool2d(xt, (6, 5)).reshape(3, 4).numpy()
+    np.testing.assert_array_equal(run1(m, f32_inputs(x))[-1], ref)
+    xr = np.maximum(x, 0)
+    for p in (1.0, 2.0, 3.0):
+        m = module("f32", [x.shape], [op("LPPOOL", [0], fp=[p])])
+        ref = torch.nn.functional.lp_pool2d(torch.from_numpy(xr.astype(np.float64)), p,
+                                            (6, 5)).reshape(3, 4).numpy()
+        np.testing.assert_allclose(run1(m, f32_inputs(xr))[-1], ref, rtol=1e-12)
+    m = module("f32", [x.shape], [op("LPPOOL", [0], fp=[1.0])])
+    np.testing.assert_allclose(run1(m, f32_inputs(xr))[-1], xr.astype(np.float64).sum((2, 3)),
+                               rtol=1e-12)
+    with pytest.raises(ValueError):
+        oracle.plan(module("f32", [x.shape], [op("LPPOOL", [0], fp=[0.0])]), [0])
+
+
 def test_layernorm_closed_form():
     eps = 1e-5
     m = module("f32", [(2, 4), (4,), (4,)], [op("LAYERNORM", [0, 1, 2], fp=[eps])])
