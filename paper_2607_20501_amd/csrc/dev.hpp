@@ -199,6 +199,24 @@ __device__ __forceinline__ void epi_apply8(const EpiDev& e, float (&v)[8], int64
   }
 }
 
+// Global pooling over positions (GAP mean, GMP max, LPPOOL sign(S)|S|^(1/p)
+// of S = sum x^p): each value's contribution, the identity and combination of
+// partial results, and the final value over `count` positions.
+__device__ __forceinline__ float pool_in(int kind, float p, float v) {
+  return kind == MK_OP_LPPOOL ? powf(v, p) : v;
+}
+__device__ __forceinline__ float pool_id(int kind) {
+  return kind == MK_OP_GMP ? -INFINITY : 0.f;
+}
+__device__ __forceinline__ float pool_comb(int kind, float a, float b) {
+  return kind == MK_OP_GMP ? fmaxf(a, b) : a + b;
+}
+__device__ __forceinline__ float pool_out(int kind, float p, float s, float count) {
+  if (kind == MK_OP_GAP) return s / count;
+  if (kind == MK_OP_LPPOOL) return copysignf(powf(fabsf(s), 1.0f / p), s);
+  return s;
+}
+
 __device__ __forceinline__ float warp_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

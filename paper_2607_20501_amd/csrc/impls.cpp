@@ -128,6 +128,8 @@ static ConvArgs conv_args(const ConvSpec& c) {
   a.N = c.N; a.C = c.C; a.H = c.H; a.W = c.W; a.K = c.K; a.R = c.R; a.S = c.S;
   a.P = c.P; a.Q = c.Q; a.stride = c.stride; a.pad = c.pad;
   a.gap = c.gap ? 1 : 0;
+  a.pool = c.pool;
+  a.pool_p = c.pool_p;
   return a;
 }
 
@@ -237,6 +239,7 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       a.eps = r.eps;
       a.pre = ew_args(r.pre, vals, nullptr, impl);
       a.n2 = r.n2;
+      a.p = r.p;
       a.variant = impl == MUT_UNSAFE_SOFTMAX      ? 1
                   : impl == MUT_SOFTMAX_WRONG_DIM ? 2
                   : impl == MUT_UNSAFE_LAYERNORM  ? 3

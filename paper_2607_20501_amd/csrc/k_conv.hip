@@ -100,22 +100,23 @@ __global__ void pack_krsc_kernel(const T* w, T* wp, int64_t K, int64_t C, int64_
   }
 }
 
-// out[n][k] = (sum of the GAP partials of the position tiles that cover image
-// n, in tile order) / PQ.  Partial (tile t, slot) holds the column sums of the
-// tile's positions in image (t*tile)/PQ + slot.
+// out[n][k] = the pool of image n from the partials of the position tiles
+// that cover it, combined in tile order (sum, or max for GMP), then finished
+// (mean over PQ, or sign(S)|S|^(1/p) for LPPOOL).  Partial (tile t, slot)
+// holds the reduction of the tile's positions in image (t*tile)/PQ + slot.
 template <typename T>
 __global__ void gap_finish_kernel(const float* partial, int64_t N, int64_t K, int64_t PQ,
-                                  int64_t tile, T* out) {
+                                  int64_t tile, int kind, float p, T* out) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= N * K) return;
   const int64_t n = i / K, k = i % K;
   const int64_t t0 = (n * PQ) / tile, t1 = ((n + 1) * PQ - 1) / tile;
-  float s = 0.f;
+  float s = pool_id(kind);
   for (int64_t t = t0; t <= t1; ++t) {
     const int64_t slot = n - (t * tile) / PQ;
-    s += partial[(t * 2 + slot) * K + k];
+    s = pool_comb(kind, s, partial[(t * 2 + slot) * K + k]);
   }
-  st<T>(out, i, s / (float)PQ);
+  st<T>(out, i, pool_out(kind, p, s, (float)PQ));
 }
 
 }  // namespace
@@ -192,6 +193,8 @@ GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float
   g.alpha = 1.f;
   g.epi = a.epi;
   g.terminal = a.gap ? TERM_GAP : TERM_NONE;
+  g.pool = a.pool;
+  g.pool_p = a.pool_p;
   g.partial = partial;
   g.n_tiles = (g.N + kConvTileN - 1) / kConvTileN;
   g.conv = 1;
@@ -210,10 +213,10 @@ hipError_t launch_gap_finish(int dtype, const ConvArgs& a, const float* partial,
   const dim3 grid((unsigned)((total + 255) / 256));
   if (dtype == MK_BF16)
     hipLaunchKernelGGL(gap_finish_kernel<bf16>, grid, dim3(256), 0, st, partial, a.N, a.K,
-                       a.P * a.Q, (int64_t)kConvTileN, (bf16*)a.y);
+                       a.P * a.Q, (int64_t)kConvTileN, (int)a.pool, a.pool_p, (bf16*)a.y);
   else
     hipLaunchKernelGGL(gap_finish_kernel<float>, grid, dim3(256), 0, st, partial, a.N, a.K,
-                       a.P * a.Q, (int64_t)kConvTileN, (float*)a.y);
+                       a.P * a.Q, (int64_t)kConvTileN, (int)a.pool, a.pool_p, (float*)a.y);
   return hipGetLastError();
 }
 

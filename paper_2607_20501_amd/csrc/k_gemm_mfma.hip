@@ -461,17 +461,19 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         // covers at most two images), then over the lanes sharing the row.
         const int64_t img0 = (n0 < a.N ? n0 : a.N - 1) / PQ;
         const bool second = row_ok && valid > 0 && img != img0;
-        float s0 = 0.f, s1 = 0.f;
+        const int kind = a.pool;
+        float s0 = pool_id(kind), s1 = pool_id(kind);
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           if (e < valid) {
-            if (second) s1 += v[e];
-            else s0 += v[e];
+            const float c = pool_in(kind, a.pool_p, v[e]);
+            if (second) s1 = pool_comb(kind, s1, c);
+            else s0 = pool_comb(kind, s0, c);
           }
 #pragma unroll
         for (int o = LPR / 2; o > 0; o >>= 1) {
-          s0 += __shfl_xor(s0, o, 64);
-          s1 += __shfl_xor(s1, o, 64);
+          s0 = pool_comb(kind, s0, __shfl_xor(s0, o, 64));
+          s1 = pool_comb(kind, s1, __shfl_xor(s1, o, 64));
         }
         if (q == 0) {
           red[(wn * 256 + lrow) * 2] = s0;
@@ -532,9 +534,9 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     if (CONV) {   // GAP partials of this position tile, per image slot
 #pragma unroll
       for (int slot = 0; slot < 2; ++slot) {
-        float ss = 0.f;
+        float ss = pool_id(a.pool);
 #pragma unroll
-        for (int g = 0; g < WN; ++g) ss += red[(g * 256 + lrow) * 2 + slot];
+        for (int g = 0; g < WN; ++g) ss = pool_comb(a.pool, ss, red[(g * 256 + lrow) * 2 + slot]);
         a.partial[((int64_t)tc.tn * 2 + slot) * a.M + row] = ss;
       }
       continue;

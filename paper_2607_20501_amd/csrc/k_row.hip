@@ -1,8 +1,9 @@
-// Tuned row kernels (HBM-bound, no element-wise prologue): one wave per row, the row held in registers
-// after one pass of 16-byte loads, reductions by wave shuffles.  Row-sum,
-// global average pool, softmax (max subtracted, App. D), LayerNorm (mean, then
-// the biased variance of the centred values; App. H.2 / App. I.2).  Each value
-// is read from HBM once and each output written once.
+// Tuned row kernels (HBM-bound, no element-wise prologue): one wave per row,
+// the row held in registers after one pass of 16-byte loads, reductions by
+// wave shuffles.  Row-sum, global average / max / LP pool, softmax (max
+// subtracted, App. D), LayerNorm (mean, then the biased variance of the
+// centred values; App. H.2 / App. I.2).  Each value is read from HBM once and
+// each output written once.
 #include "dev.hpp"
 
 namespace mk {
@@ -51,6 +52,18 @@ __global__ __launch_bounds__(256) void row_wave_kernel(RowArgs a) {
     const int64_t c = (int64_t)(i * 64 + lane) * E;
     ok[i] = c < L;
     if (ok[i]) ld_vec<T>(x + c, v[i]);
+  }
+  if (a.op == MK_OP_GMP || a.op == MK_OP_LPPOOL) {
+    const int kind = a.op;
+    float s = pool_id(kind);
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (ok[i])
+#pragma unroll
+        for (int k = 0; k < E; ++k) s = pool_comb(kind, s, pool_in(kind, a.p, v[i][k]));
+    s = kind == MK_OP_GMP ? warp_max(s) : warp_sum(s);
+    if (lane == 0) st<T>((T*)a.y, r, pool_out(kind, a.p, s, (float)L));
+    return;
   }
   if (a.op == MK_OP_ROWSUM || a.op == MK_OP_GAP) {
     float s = 0.f;

@@ -145,6 +145,15 @@ __global__ __launch_bounds__(256) void row_kernel(RowArgs a) {
       if (threadIdx.x == 0) st<T>((T*)a.y, r, a.op == MK_OP_GAP ? s / (float)L : s);
       break;
     }
+    case MK_OP_GMP: case MK_OP_LPPOOL: {
+      const int kind = a.op;
+      float s = pool_id(kind);
+      for (int64_t j = threadIdx.x; j < L; j += blockDim.x)
+        s = pool_comb(kind, s, pool_in(kind, a.p, row_in<T>(a, r, j)));
+      s = kind == MK_OP_GMP ? block_max(s, red) : block_sum(s, red);
+      if (threadIdx.x == 0) st<T>((T*)a.y, r, pool_out(kind, a.p, s, (float)L));
+      break;
+    }
     case MK_OP_SOFTMAX: {
       float m = -INFINITY;
       for (int64_t j = threadIdx.x; j < L; j += blockDim.x) m = fmaxf(m, row_in<T>(a, r, j));
@@ -473,19 +482,21 @@ __global__ void conv_simple_kernel(ConvArgs a) {
   }
 }
 
-// Conv + chain + global average pool: one workgroup per (image, channel).
+// Conv + chain + global pool: one workgroup per (image, channel).
 template <typename T>
 __global__ __launch_bounds__(256) void conv_gap_simple_kernel(ConvArgs a) {
   __shared__ float red[16];
   const int64_t nk = blockIdx.x, n = nk / a.K, k = nk % a.K;
   const int64_t PQ = a.P * a.Q;
-  float s = 0.f;
+  const int kind = a.pool;
+  float s = pool_id(kind);
   for (int64_t pos = threadIdx.x; pos < PQ; pos += blockDim.x) {
     float v = conv_at<T>(a, n, k, pos / a.Q, pos % a.Q);
-    s += epi_apply<T>(a.epi, v, 0, 0, k, nk * PQ + pos);
+    v = epi_apply<T>(a.epi, v, 0, 0, k, nk * PQ + pos);
+    s = pool_comb(kind, s, pool_in(kind, a.pool_p, v));
   }
-  s = block_sum(s, red);
-  if (threadIdx.x == 0) st<T>((T*)a.y, nk, s / (float)PQ);
+  s = kind == MK_OP_GMP ? block_max(s, red) : block_sum(s, red);
+  if (threadIdx.x == 0) st<T>((T*)a.y, nk, pool_out(kind, a.pool_p, s, (float)PQ));
 }
 
 hipError_t launch_conv_simple(int dtype, const ConvArgs& a, hipStream_t st) {

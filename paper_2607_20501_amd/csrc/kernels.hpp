@@ -39,6 +39,7 @@ struct RowArgs {
   // 3 LayerNorm without the mean subtracted before scaling.
   int32_t variant;
   int64_t n2;
+  float p;                 // LPPOOL exponent
 };
 
 struct GemmArgs {
@@ -63,6 +64,8 @@ struct GemmArgs {
   // (terminal == TERM_GAP: partial[(tile * 2 + slot) * M + k]).
   int32_t conv;
   int64_t cv_C, cv_Hp, cv_Wp, cv_P, cv_Q, cv_S, cv_stride;
+  int32_t pool;            // kind of the global pool of TERM_GAP (GAP, GMP, LPPOOL)
+  float pool_p;
 };
 
 struct ConvArgs {
@@ -71,7 +74,9 @@ struct ConvArgs {
   void* y;
   int64_t N, C, H, W, K, R, S, P, Q, stride, pad;
   EpiDev epi;              // channel-indexed chain
-  int32_t gap;
+  int32_t gap;             // ends in a global pool of kind pool (GAP, GMP, LPPOOL)
+  int32_t pool;
+  float pool_p;
   float* partial;          // GAP partial sums [N][K][n_pos_tiles]
   int64_t n_pos_tiles;
   void* scratch;           // tuned conv: repacked operands

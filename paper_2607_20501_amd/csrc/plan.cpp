@@ -138,8 +138,10 @@ mk_status infer(const mk_module_desc* d, std::vector<mk_shape>& vs) {
         y = make_shape({x.dims[0], w.dims[0], hp / st + 1, wp / st + 1});
         break;
       }
-      case MK_OP_GAP:
-        if (x.ndim != 4) return fail(MK_E_SHAPE, where + "GAP needs [N,C,H,W]");
+      case MK_OP_GAP: case MK_OP_GMP: case MK_OP_LPPOOL:
+        if (x.ndim != 4) return fail(MK_E_SHAPE, where + "global pool needs [N,C,H,W]");
+        if (o.kind == MK_OP_LPPOOL && !(o.fp[0] > 0.0))
+          return fail(MK_E_SHAPE, where + "LPPOOL needs p > 0");
         y = make_shape({x.dims[0], x.dims[1]});
         break;
       case MK_OP_QK: case MK_OP_PV: {
@@ -392,8 +394,11 @@ bool match_group(const Plan& p, int32_t b, int32_t e, Subkernel& sk, std::string
     cs.stride = first.ip[0];
     cs.pad = first.ip[1];
     for (int i = b + 1; i < e; ++i) {
-      if (p.ops[i].kind == MK_OP_GAP && i == e - 1) {
+      const int32_t k = p.ops[i].kind;
+      if ((k == MK_OP_GAP || k == MK_OP_GMP || k == MK_OP_LPPOOL) && i == e - 1) {
         cs.gap = true;
+        cs.pool = k;
+        cs.pool_p = k == MK_OP_LPPOOL ? (float)p.ops[i].fp[0] : 1.f;
         continue;
       }
       if (!push_step(p, i, vb, ve, 3, cs.epi, why)) return false;
@@ -406,8 +411,10 @@ bool match_group(const Plan& p, int32_t b, int32_t e, Subkernel& sk, std::string
   // Row family: element-wise prologue, then one row op.
   {
     const mk_op& last = p.ops[e - 1];
+    const bool pool = last.kind == MK_OP_GAP || last.kind == MK_OP_GMP ||
+                      last.kind == MK_OP_LPPOOL;
     if (last.kind == MK_OP_ROWSUM || last.kind == MK_OP_SOFTMAX || last.kind == MK_OP_LAYERNORM ||
-        last.kind == MK_OP_GAP) {
+        pool) {
       RowSpec r;
       r.x_value = first.in[0];
       const mk_shape& x = p.vshape[r.x_value];
@@ -417,9 +424,10 @@ bool match_group(const Plan& p, int32_t b, int32_t e, Subkernel& sk, std::string
         if (!push_step(p, i, vb, ve, 0, r.pre.epi, why)) return false;
       r.op = last.kind;
       const mk_shape& xin = p.vshape[last.in[0]];
-      if (last.kind == MK_OP_GAP) {
+      if (pool) {
         r.len = xin.dims[2] * xin.dims[3];
         r.rows = xin.dims[0] * xin.dims[1];
+        r.p = last.kind == MK_OP_LPPOOL ? (float)last.fp[0] : 1.f;
       } else {
         r.len = xin.dims[xin.ndim - 1];
         r.rows = numel(xin) / r.len;

@@ -56,7 +56,9 @@ struct ConvSpec {
   int32_t x_value = -1, w_value = -1;
   int64_t N = 0, C = 0, H = 0, W = 0, K = 0, R = 0, S = 0, P = 0, Q = 0, stride = 1, pad = 0;
   EpiChain epi;          // channel-indexed chain
-  bool gap = false;
+  bool gap = false;      // ends in a global pool
+  int32_t pool = MK_OP_GAP;   // GAP, GMP or LPPOOL
+  float pool_p = 1.f;         // LPPOOL exponent
 };
 
 struct EwSpec {
@@ -76,6 +78,7 @@ struct RowSpec {
   int32_t g_value = -1, b_value = -1;
   float eps = 0.f;
   int64_t n2 = 1;              // size of the input's dim -2 (1 for a vector)
+  float p = 1.f;               // LPPOOL exponent
 };
 
 struct AttnSpec {

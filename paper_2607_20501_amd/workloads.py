@@ -46,16 +46,19 @@ def gemm_gelu_softmax(M=8192, K=4096, N=4096, dtype="bf16", scale=0.5):
     }
 
 
-def conv_relu_gap(N=64, C=128, H=56, W=56, K=256, R=3, stride=1, pad=1, dtype="bf16"):
-    """3x3 conv (NCHW, KCRS) + per-channel bias + ReLU + global average pool;
-    x ~ N(0, 1), w ~ N(0, 0.02), b ~ U(-0.1, 0.1)."""
+def conv_relu_gap(N=64, C=128, H=56, W=56, K=256, R=3, stride=1, pad=1, dtype="bf16",
+                  pool="GAP", p=2.0):
+    """3x3 conv (NCHW, KCRS) + per-channel bias + ReLU + global pool: average
+    (GAP), or the variants of Sec. 4's MobileNet adaptation, max (GMP) and
+    LP with exponent p (LPPOOL); x ~ N(0, 1), w ~ N(0, 0.02), b ~ U(-0.1, 0.1)."""
+    tag = {"GAP": "gap", "GMP": "gmp", "LPPOOL": f"lp{p:g}"}[pool]
     return {
-        "name": f"conv_relu_gap_{N}x{C}x{H}x{W}_k{K}_{dtype}",
+        "name": f"conv_relu_{tag}_{N}x{C}x{H}x{W}_k{K}_{dtype}",
         "dtype": dtype,
         "inputs": [[N, C, H, W], [K, C, R, R], [K]],
         "recipes": [(NORMAL, 0.0, 1.0), (NORMAL, 0.0, 0.02), (UNIFORM, -0.1, 0.1)],
         "ops": [_op("CONV2D", [0, 1], [stride, pad]), _op("BIAS_CHANNEL", [3, 2]),
-                _op("RELU", [4]), _op("GAP", [5])],
+                _op("RELU", [4]), _op(pool, [5], fp=[p] if pool == "LPPOOL" else [])],
     }
 
 

@@ -36,3 +36,24 @@ def test_conv_impls_agree():
     rep, m, *_ = run_parity(module, "fused")
     assert rep["pass"], describe(rep)
     assert m.subkernels()[0]["n_launches"] == 4
+
+
+POOL_CASES = [dict(N=3, C=32, H=20, W=20, K=40), dict(N=2, C=64, H=16, W=16, K=300),
+              dict(N=2, C=8, H=9, W=7, K=5)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("pool,p", [("GMP", 2.0), ("LPPOOL", 2.0), ("LPPOOL", 3.0)])
+@pytest.mark.parametrize("shape", POOL_CASES)
+@pytest.mark.parametrize("dec", ["fused", "split"])
+def test_pooling_variants(shape, dec, pool, p, dtype):
+    """Max and LP pooling in place of the average (Sec. 4 adaptation): fused
+    into the conv GEMM's per-tile partials (tiles straddle images) and as a
+    row subkernel after the split conv."""
+    print(f"conv {shape} {dec} {pool} p={p} {dtype}", flush=True)
+    module = workloads.conv_relu_gap(dtype=dtype, pool=pool, p=p, **shape)
+    rep, m, *_ = run_parity(module, dec)
+    assert rep["pass"], describe(rep)
+    for impl in (mk.IMPL_SIMPLE,):
+        rep, *_ = run_parity(module, dec, impls={i: impl for i in range(m.n)})
+        assert rep["pass"], "simple: " + describe(rep)

@@ -96,6 +96,51 @@ def test_bookkeeping_matches_oracle_for_every_accepted_grouping(k):
         assert accepted >= 2
 
 
+def check_all_groupings(module):
+    n = len(module["ops"])
+    accepted = 0
+    for g in groupings(n):
+        try:
+            h = mk.mk_module_create(module, g)
+        except mk.MkError as e:
+            assert e.status == 4, str(e)
+            continue
+        accepted += 1
+        try:
+            ref = oracle.plan(module, g)
+            info = mk.mk_module_info(h)
+            assert (info["n_subkernels"], info["flops"], info["alg_bytes"]) == \
+                (len(ref["groups"]), ref["flops"], ref["alg_bytes"])
+            for i, rg in enumerate(ref["groups"]):
+                s = mk.mk_subkernel_info(h, i)
+                for f in FIELDS:
+                    assert s[f] == rg[f], (g, i, f, s[f], rg[f])
+        finally:
+            mk.mk_module_destroy(h)
+    return accepted
+
+
+@pytest.mark.parametrize("pool", ["GMP", "LPPOOL"])
+def test_pooling_variants_plan_like_gap(pool):
+    """Sec. 4's MobileNet adaptation: replacing average pooling by max or LP
+    pooling swaps one subkernel.  Every grouping the GAP module accepts is
+    accepted with the same bookkeeping, the conv subkernel of the split form
+    is unchanged, and the fused form still ends in the conv subkernel."""
+    for kw in ({}, dict(N=2, C=5, H=9, W=7, K=6)):
+        gap = workloads.conv_relu_gap(**kw)
+        var = workloads.conv_relu_gap(pool=pool, p=3.0, **kw)
+        assert check_all_groupings(var) == check_all_groupings(gap)
+        for dec in ("split", "fused"):
+            assert mk.mk_decomposition_preset(var, dec) == mk.mk_decomposition_preset(gap, dec)
+        a, b = mk.Module(gap, "split").subkernels(), mk.Module(var, "split").subkernels()
+        assert a[:-1] == b[:-1]
+        assert b[-1]["family"] == a[-1]["family"] == "ROW"
+        assert [s["family"] for s in mk.Module(var, "fused").subkernels()] == ["CONV"]
+    with pytest.raises(mk.MkError):
+        mk.mk_module_create(workloads.conv_relu_gap(N=1, C=4, H=5, W=5, K=3, pool="LPPOOL",
+                                                    p=0.0), [0, 0, 0, 0])
+
+
 def test_hand_computed_full_size_integers():
     c2 = mk.Module(FULL[1], "fused")
     assert c2.info["flops"] == 2 * 8192 * 4096 * 4096 == 274877906944
