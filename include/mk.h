@@ -142,8 +142,9 @@ typedef struct {
 
 /* Fill group_of_op[n_ops] with a preset decomposition.  preset 0 = split (one
  * subkernel per op, except that a BIAS, BIAS_CHANNEL or ADD joins the GEMM or
- * CONV2D that produces its input); preset 1 = fused (from each op, the longest
- * group a family accepts).  Host only. */
+ * CONV2D that produces its input, directly or through bias / add steps that
+ * joined it); preset 1 = fused (from each op, the longest group a family
+ * accepts).  Host only. */
 mk_status mk_decomposition_preset(const mk_module_desc* desc, int32_t preset,
                                   int32_t* group_of_op);
 

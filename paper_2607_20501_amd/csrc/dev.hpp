@@ -217,6 +217,28 @@ __device__ __forceinline__ float pool_out(int kind, float p, float s, float coun
   return s;
 }
 
+// Row moments (count, mean, sum of squared deviations M2): Welford's update
+// for one value, Chan et al.'s pairwise combination for two partial results
+// (no E[x^2] - mean^2 cancellation).
+struct Moments {
+  float n, mean, m2;
+};
+__device__ __forceinline__ void mom_add(Moments& a, float v) {
+  a.n += 1.f;
+  const float d = v - a.mean;
+  a.mean += d / a.n;
+  a.m2 += d * (v - a.mean);
+}
+__device__ __forceinline__ Moments mom_comb(const Moments& a, const Moments& b) {
+  const float n = a.n + b.n;
+  if (n == 0.f) return a;
+  const float d = b.mean - a.mean, f = b.n / n;
+  return {n, a.mean + d * f, a.m2 + b.m2 + d * d * a.n * f};
+}
+__device__ __forceinline__ Moments mom_shfl_xor(const Moments& a, int o) {
+  return {__shfl_xor(a.n, o, 64), __shfl_xor(a.mean, o, 64), __shfl_xor(a.m2, o, 64)};
+}
+
 __device__ __forceinline__ float warp_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -119,7 +119,8 @@ static GemmScratch gemm_scratch(const Plan& p, const Subkernel& sk, int impl) {
   if (g.ln) s.ln_bytes = align256(s.mfma ? g.M * g.K * elem_size(p.dtype) : 2 * g.M * 4);
   if (s.mfma && g.layout == 1) s.bt_bytes = align256(g.batch * g.heads * g.N * g.K * elem_size(p.dtype));
   if (g.terminal == TERM_ROWSUM) s.partial_bytes = align256(g.M * s.n_tiles * 4);
-  if (g.terminal == TERM_SOFTMAX) s.partial_bytes = align256(g.M * s.n_tiles * 8);
+  if (g.terminal == TERM_SOFTMAX || g.terminal == TERM_LAYERNORM)
+    s.partial_bytes = align256(g.M * s.n_tiles * 8);
   return s;
 }
 
@@ -321,6 +322,13 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
                            return launch_rowsum_finish(dt, a.partial, g.M, a.n_tiles, out, st);
                          }),
                          "row-sum finish");
+      if (g.terminal == TERM_LAYERNORM)
+        return hip_check(timed([&] {
+                           return launch_ln_finish(dt, a.partial, g.M, a.n_tiles, g.N,
+                                                   gs.mfma ? kGemmTileN : 64, vals[g.post_g],
+                                                   vals[g.post_b], g.post_eps, out, st);
+                         }),
+                         "layernorm finish");
       if (g.terminal == TERM_SOFTMAX)
         return hip_check(timed([&] {
                            return launch_softmax_finish(dt, a.partial, g.M, a.n_tiles, g.N, out,

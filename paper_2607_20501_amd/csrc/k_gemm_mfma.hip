@@ -450,7 +450,9 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok));
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX) v[e] = rnd<T>(v[e]);
+        if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX ||
+            a.terminal == TERM_LAYERNORM)
+          v[e] = rnd<T>(v[e]);
         if (e < valid) {
           m = fmaxf(m, v[e]);
           sum += v[e];
@@ -493,7 +495,19 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
             if (e < valid) st<T>(C, off + e, v[e]);
         }
       }
-      if (a.terminal != TERM_NONE) {
+      if (a.terminal == TERM_LAYERNORM) {
+        // moments of this wave's columns of the row (values as stored)
+        Moments mo{0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e < valid) mom_add(mo, v[e]);
+#pragma unroll
+        for (int o = LPR / 2; o > 0; o >>= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
+        if (q == 0) {
+          red[(wn * 256 + lrow) * 2] = mo.mean;
+          red[(wn * 256 + lrow) * 2 + 1] = mo.m2;
+        }
+      } else if (a.terminal != TERM_NONE) {
         // reduce over the LPR lanes that share this row (this wave's columns)
         if (softmax) {
 #pragma unroll
@@ -541,8 +555,20 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       }
       continue;
     }
-    float* part = a.partial + (row * a.n_tiles + tc.tn) * (softmax ? 2 : 1);
-    if (softmax) {
+    float* part = a.partial +
+                  (row * a.n_tiles + tc.tn) * (softmax || a.terminal == TERM_LAYERNORM ? 2 : 1);
+    if (a.terminal == TERM_LAYERNORM) {
+      // combine the WN waves' column ranges (their counts follow from N)
+      Moments acc{0.f, 0.f, 0.f};
+#pragma unroll
+      for (int g = 0; g < WN; ++g) {
+        const int64_t c0 = n0 + g * WTN;
+        const float cnt = (float)min<int64_t>(WTN, max<int64_t>(0, a.N - c0));
+        acc = mom_comb(acc, Moments{cnt, red[(g * 256 + lrow) * 2], red[(g * 256 + lrow) * 2 + 1]});
+      }
+      part[0] = acc.mean;
+      part[1] = acc.m2;
+    } else if (softmax) {
       float mm = -INFINITY;
 #pragma unroll
       for (int g = 0; g < WN; ++g) mm = fmaxf(mm, red[(g * 256 + lrow) * 2]);

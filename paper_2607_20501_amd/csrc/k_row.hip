@@ -188,7 +188,61 @@ __global__ __launch_bounds__(256) void softmax_finish_wave_kernel(const float* p
   }
 }
 
+// LayerNorm finisher over the per-(row, column tile) moments (mean_t, M2_t) of
+// a GEMM epilogue (tile t holds min(tile, N - t*tile) columns): the moments
+// are merged (Chan et al.), then the stored row is normalised in place,
+// y = (x - mean) / sqrt(M2 / N + eps) * gamma + beta.  One wave per row.
+template <typename T>
+__global__ __launch_bounds__(256) void ln_finish_wave_kernel(const float* partial, int64_t rows,
+                                                             int64_t nt, int64_t N, int64_t tile,
+                                                             const T* gamma, const T* beta,
+                                                             float eps, T* out) {
+  constexpr int E = kEpv<T>;
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;   // whole wave exits together
+  const float* pr = partial + r * nt * 2;
+  Moments mo{0.f, 0.f, 0.f};
+  for (int64_t t = lane; t < nt; t += 64) {
+    const float cnt = (float)min<int64_t>(tile, N - t * tile);
+    mo = mom_comb(mo, Moments{cnt, pr[t * 2], pr[t * 2 + 1]});
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
+  const float mean = mo.mean, rstd = rsqrtf(mo.m2 / (float)N + eps);
+  T* y = out + r * N;
+  const bool vec = N % E == 0 && ((uintptr_t)out | (uintptr_t)gamma | (uintptr_t)beta) % 16 == 0;
+  if (vec) {
+    for (int64_t c = lane; c < N / E; c += 64) {
+      float v[E], g[E], b[E];
+      ld_vec<T>(y + c * E, v);
+      ld_vec<T>(gamma + c * E, g);
+      ld_vec<T>(beta + c * E, b);
+#pragma unroll
+      for (int k = 0; k < E; ++k) v[k] = (v[k] - mean) * rstd * g[k] + b[k];
+      st_vec<T>(y + c * E, v);
+    }
+  } else {
+    for (int64_t j = lane; j < N; j += 64)
+      st<T>(y, j, (ld<T>(y, j) - mean) * rstd * ld<T>(gamma, j) + ld<T>(beta, j));
+  }
+}
+
 }  // namespace
+
+hipError_t launch_ln_finish(int dtype, const float* partial, int64_t rows, int64_t nt, int64_t N,
+                            int64_t tile, const void* gamma, const void* beta, float eps,
+                            void* out, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+  if (dtype == MK_BF16)
+    hipLaunchKernelGGL(ln_finish_wave_kernel<bf16>, grid, block, 0, st, partial, rows, nt, N, tile,
+                       (const bf16*)gamma, (const bf16*)beta, eps, (bf16*)out);
+  else
+    hipLaunchKernelGGL(ln_finish_wave_kernel<float>, grid, block, 0, st, partial, rows, nt, N,
+                       tile, (const float*)gamma, (const float*)beta, eps, (float*)out);
+  return hipGetLastError();
+}
 
 bool softmax_finish_wave_supported(int dtype, int64_t N, const void* out) {
   const int E = dtype == MK_BF16 ? 8 : 4;

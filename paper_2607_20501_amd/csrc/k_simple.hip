@@ -340,6 +340,7 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmArgs a) {
   for (int i = 0; i < 4; ++i) {
     const int64_t gm = m0 + ty * 4 + i;
     float rs = 0.f, rm = -INFINITY, re = 0.f;
+    Moments mo{0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int64_t gn = n0 + tx * 4 + j;
@@ -354,6 +355,10 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmArgs a) {
           const float nm = fmaxf(rm, v);
           re = re * __expf(rm - nm) + __expf(v - nm);
           rm = nm;
+        } else if (a.terminal == TERM_LAYERNORM) {
+          v = rnd<T>(v);
+          st<T>(C, gm * a.ldc + gn, v);
+          mom_add(mo, v);
         } else {
           st<T>(C, gm * a.ldc + gn, v);
         }
@@ -376,6 +381,13 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmArgs a) {
       if (tx == 0 && gm < a.M) {
         a.partial[(gm * a.n_tiles + blockIdx.x) * 2] = rm;
         a.partial[(gm * a.n_tiles + blockIdx.x) * 2 + 1] = re;
+      }
+    } else if (a.terminal == TERM_LAYERNORM) {
+#pragma unroll
+      for (int o = 8; o > 0; o >>= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
+      if (tx == 0 && gm < a.M) {
+        a.partial[(gm * a.n_tiles + blockIdx.x) * 2] = mo.mean;
+        a.partial[(gm * a.n_tiles + blockIdx.x) * 2 + 1] = mo.m2;
       }
     }
   }

@@ -114,6 +114,10 @@ hipError_t launch_attn_simple(int dtype, const AttnArgs& a, hipStream_t st);
 // arithmetic; ew_fast_supported() states when it applies.
 bool ew_fast_supported(const EwArgs& a);
 bool softmax_finish_wave_supported(int dtype, int64_t N, const void* out);
+// Post-LN finisher for TERM_LAYERNORM (per-tile moments of `tile` columns).
+hipError_t launch_ln_finish(int dtype, const float* partial, int64_t rows, int64_t nt, int64_t N,
+                            int64_t tile, const void* gamma, const void* beta, float eps,
+                            void* out, hipStream_t st);
 hipError_t launch_softmax_finish_wave(int dtype, const float* partial, int64_t rows, int64_t nt,
                                       int64_t N, void* out, hipStream_t st);
 hipError_t launch_ew_fast(int dtype, const EwArgs& a, hipStream_t st);

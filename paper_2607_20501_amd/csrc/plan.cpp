@@ -311,7 +311,7 @@ bool match_group(const Plan& p, int32_t b, int32_t e, Subkernel& sk, std::string
     }
   }
 
-  // GEMM family: [LAYERNORM] GEMM|QK|PV, epilogue, [ROWSUM|SOFTMAX].
+  // GEMM family: [LAYERNORM] GEMM|QK|PV, epilogue, [ROWSUM|SOFTMAX|LAYERNORM].
   {
     int i = b;
     GemmSpec g;
@@ -365,8 +365,16 @@ bool match_group(const Plan& p, int32_t b, int32_t e, Subkernel& sk, std::string
       bool ok = true;
       for (; i < e && ok; ++i) {
         const int32_t k = p.ops[i].kind;
-        if ((k == MK_OP_ROWSUM || k == MK_OP_SOFTMAX) && i == e - 1 && c.kind == MK_OP_GEMM) {
-          g.terminal = k == MK_OP_ROWSUM ? TERM_ROWSUM : TERM_SOFTMAX;
+        if ((k == MK_OP_ROWSUM || k == MK_OP_SOFTMAX || k == MK_OP_LAYERNORM) && i == e - 1 &&
+            c.kind == MK_OP_GEMM) {
+          g.terminal = k == MK_OP_ROWSUM    ? TERM_ROWSUM
+                       : k == MK_OP_SOFTMAX ? TERM_SOFTMAX
+                                            : TERM_LAYERNORM;
+          if (k == MK_OP_LAYERNORM) {
+            g.post_g = p.ops[i].in[1];
+            g.post_b = p.ops[i].in[2];
+            g.post_eps = (float)p.ops[i].fp[0];
+          }
           continue;
         }
         ok = push_step(p, i, vb, ve, ctx, g.epi, why);
@@ -552,14 +560,18 @@ mk_status preset(const mk_module_desc* d, int32_t which, int32_t* out) {
   const int nops = d->n_ops;
   std::vector<int32_t> g(nops);
   if (which == 0) {
+    // A bias or residual add joins the contraction that produces its input,
+    // directly or through bias / add steps that already joined it.
     int gi = 0;
+    std::vector<char> joined(nops, 0);
     for (int i = 0; i < nops; ++i) {
       const int32_t k = p.ops[i].kind;
-      const bool joins = i > 0 &&
-                         (k == MK_OP_BIAS || k == MK_OP_BIAS_CHANNEL || k == MK_OP_ADD) &&
-                         (p.ops[i - 1].kind == MK_OP_GEMM || p.ops[i - 1].kind == MK_OP_CONV2D) &&
-                         p.ops[i].in[0] == p.n_inputs + i - 1 && g[i - 1] == gi;
-      if (i > 0 && !joins) ++gi;
+      const bool after_contraction =
+          i > 0 && (p.ops[i - 1].kind == MK_OP_GEMM || p.ops[i - 1].kind == MK_OP_CONV2D ||
+                    joined[i - 1]);
+      joined[i] = i > 0 && (k == MK_OP_BIAS || k == MK_OP_BIAS_CHANNEL || k == MK_OP_ADD) &&
+                  after_contraction && p.ops[i].in[0] == p.n_inputs + i - 1 && g[i - 1] == gi;
+      if (i > 0 && !joined[i]) ++gi;
       g[i] = gi;
     }
   } else {

@@ -50,6 +50,8 @@ struct GemmSpec {
   float alpha = 1.f;
   EpiChain epi;
   int32_t terminal = TERM_NONE;
+  int32_t post_g = -1, post_b = -1;   // TERM_LAYERNORM gamma / beta value ids
+  float post_eps = 0.f;
 };
 
 struct ConvSpec {

@@ -21,6 +21,15 @@ enum EpiCode : int32_t {
 };
 constexpr int kMaxEpi = 8;
 
-enum Terminal : int32_t { TERM_NONE = 0, TERM_ROWSUM = 1, TERM_SOFTMAX = 2, TERM_GAP = 3 };
+// Terminal reductions that need a whole row (or image) and are split at the
+// GEMM's column tile: per-tile partials, then a finisher.  TERM_LAYERNORM is
+// the post-LN "residual + LayerNorm" ending of a CvT-style block.
+enum Terminal : int32_t {
+  TERM_NONE = 0,
+  TERM_ROWSUM = 1,
+  TERM_SOFTMAX = 2,
+  TERM_GAP = 3,
+  TERM_LAYERNORM = 4
+};
 
 }  // namespace mk

@@ -109,6 +109,28 @@ def transformer_layer(B=8, S=2048, D=2048, H=16, F=8192, dtype="bf16", eps=1e-5,
     }
 
 
+def cvt_ffn_block(M=4096, D=768, F=3072, dtype="bf16", eps=1e-5):
+    """Post-LN ReLU FFN of a CvT block (App. H.2): out = LN(x + W2 relu(W1 x +
+    b1) + b2).  x ~ N(0, 1); W ~ N(0, 0.02); b ~ U(-0.1, 0.1); gamma ~
+    U(0.5, 1.5), beta ~ U(-0.5, 0.5)."""
+    w, bias = (NORMAL, 0.0, 0.02), (UNIFORM, -0.1, 0.1)
+    n = 7
+    return {
+        "name": f"cvt_ffn_{M}x{D}x{F}_{dtype}",
+        "dtype": dtype,
+        "inputs": [[M, D], [F, D], [F], [D, F], [D], [D], [D]],
+        "recipes": [(NORMAL, 0.0, 1.0), w, bias, w, bias, (UNIFORM, 0.5, 1.5),
+                    (UNIFORM, -0.5, 0.5)],
+        "ops": [_op("GEMM", [0, 1], [0]),                      # 0
+                _op("BIAS", [n + 0, 2]),                        # 1
+                _op("RELU", [n + 1]),                           # 2
+                _op("GEMM", [n + 2, 3], [0]),                   # 3
+                _op("BIAS", [n + 3, 4]),                        # 4
+                _op("ADD", [n + 4, 0]),                         # 5 residual
+                _op("LAYERNORM", [n + 5, 5, 6], fp=[eps])],     # 6 post-LN
+    }
+
+
 def causal_attention_block(B=2, S=256, D=512, H=4, dtype="bf16", x_std=1.0):
     """MinGPT-style causal self-attention without residual (App. D case 1):
     QKV projection -> scaled q.k -> causal mask -> softmax -> PV -> output

@@ -153,3 +153,21 @@ def test_linear_relu_rowsum_f32_both_impls():
             rep, m, *_ = run_parity(module, g, impls={i: impl for i in range(max(g) + 1)})
             assert rep["pass"], f"{dec} impl {impl}: " + describe(rep)
             assert m.subkernels()[0]["uses_mfma"] == (impl == mk.IMPL_TUNED)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dec", ["fused", "split"])
+@pytest.mark.parametrize("shape", [(300, 256, 512), (257, 600, 264), (64, 1000, 128)])
+def test_post_ln_ffn_block(shape, dec, dtype):
+    """CvT post-LN ReLU FFN, LN(x + W2 relu(W1 x + b1) + b2): fused, the
+    second GEMM ends in the LayerNorm terminal (per-tile moments, then the
+    finisher); ragged row lengths leave partial column tiles."""
+    M, D, F = shape
+    print(f"cvt ffn {shape} {dec} {dtype}", flush=True)
+    module = workloads.cvt_ffn_block(M=M, D=D, F=F, dtype=dtype)
+    rep, m, *_ = run_parity(module, dec)
+    assert rep["pass"], describe(rep)
+    if dec == "fused":
+        assert m.subkernels()[1]["uses_mfma"] and m.subkernels()[1]["n_launches"] == 2
+    rep, *_ = run_parity(module, dec, impls={i: mk.IMPL_SIMPLE for i in range(m.n)})
+    assert rep["pass"], "simple: " + describe(rep)

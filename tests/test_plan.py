@@ -141,6 +141,19 @@ def test_pooling_variants_plan_like_gap(pool):
                                                     p=0.0), [0, 0, 0, 0])
 
 
+def test_post_ln_block_plans():
+    """The CvT post-LN FFN: the split form keeps the LayerNorm as a row
+    subkernel; the fused form ends the second GEMM with it (a terminal that
+    needs the whole row, like softmax)."""
+    for m in (workloads.cvt_ffn_block(), workloads.cvt_ffn_block(M=37, D=100, F=72)):
+        assert mk.mk_decomposition_preset(m, "split") == [0, 0, 1, 2, 2, 2, 3]
+        assert mk.mk_decomposition_preset(m, "fused") == [0, 0, 0, 1, 1, 1, 1]
+        f = mk.Module(m, "fused").subkernels()
+        assert [s["family"] for s in f] == ["GEMM", "GEMM"]
+        assert f[1]["n_launches"] == 2            # GEMM + LayerNorm finisher
+        assert check_all_groupings(m) >= 8
+
+
 def test_hand_computed_full_size_integers():
     c2 = mk.Module(FULL[1], "fused")
     assert c2.info["flops"] == 2 * 8192 * 4096 * 4096 == 274877906944
