@@ -49,14 +49,18 @@ def launch_names(mod):
         n = s["n_launches"]
         if s["family"] == "GEMM":
             ln = ops[0] == "LAYERNORM"
-            fin = ops[-1] in ("SOFTMAX", "ROWSUM")
+            fin = ops[-1] in ("SOFTMAX", "ROWSUM", "LAYERNORM")
             seq = ["row_kernel (layernorm prologue)"] if ln else []
             if n - len(seq) - (2 if fin else 1) == 1:
                 seq.append("transpose_b_kernel")
-            seq.append("gemm_bf16_mfma_kernel (" + ",".join(ops) + ")")
+            seq.append("gemm_mfma_kernel (" + ",".join(ops) + ")")
             if fin:
                 seq.append(ops[-1].lower() + "_finish_kernel")
             names += seq
+        elif s["family"] == "CONV" and n >= 3:
+            names += ["pack_nhwc_kernel", "pack_krsc_kernel",
+                      "gemm_mfma_kernel (conv: " + ",".join(ops) + ")"]
+            names += ["gap_finish_kernel"] * (n - 3)
         elif s["family"] == "ATTN":
             names += ["attn_fwd_kernel (" + ",".join(ops) + ")"] * n
         else:

@@ -231,8 +231,7 @@ __device__ __forceinline__ void mom_add(Moments& a, float v) {
 }
 __device__ __forceinline__ Moments mom_comb(const Moments& a, const Moments& b) {
   const float n = a.n + b.n;
-  if (n == 0.f) return a;
-  const float d = b.mean - a.mean, f = b.n / n;
+  const float d = b.mean - a.mean, f = n > 0.f ? b.n / n : 0.f;   // (n = 0: both empty)
   return {n, a.mean + d * f, a.m2 + b.m2 + d * d * a.n * f};
 }
 __device__ __forceinline__ Moments mom_shfl_xor(const Moments& a, int o) {

@@ -426,6 +426,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   // 16-byte accesses to C and to residual operands need 8-aligned offsets.
   const bool vec_ok = ((a.ldc | cbase) & 7) == 0;
   const int valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
+  // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0); the tile
+  // covers at most two, and slot 1 is the second.
+  const int64_t img = CONV ? col0 / PQ : 0;
+  const bool second = CONV && valid > 0 && img != (n0 < a.N ? n0 : a.N - 1) / PQ;
 
   auto finish_slab = [&](int i) {
     __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): slab writes done (wave-private)
@@ -438,40 +442,36 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       const float4 hi = *(const float4*)(slab + rl * LD + q * 8 + 4);
       float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
       const bool row_ok = row < a.M;
-      float m = -INFINITY, sum = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] *= a.alpha;
       // Offset of (row, col0) in the output: row-major, or NCHW for a conv
-      // (row = channel, col = position; PQ % 8 == 0 keeps the 8 in one image).
-      const int64_t img = CONV ? col0 / PQ : 0;
+      // (row = channel, col = position).
       const int64_t obase = CONV ? (img * a.M + row) * PQ + (col0 - img * PQ)
                                  : cbase + row * a.ldc + col0;
       if (a.epi.n && row_ok && valid > 0)
         epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok));
+      // Stored values are rounded to the storage type; reductions that need
+      // the whole row read them back as stored.  Below, lanes past N take
+      // part through selects, not branches.
+      if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX || a.terminal == TERM_LAYERNORM)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX ||
-            a.terminal == TERM_LAYERNORM)
-          v[e] = rnd<T>(v[e]);
-        if (e < valid) {
-          m = fmaxf(m, v[e]);
-          sum += v[e];
-        }
-      }
+        for (int e = 0; e < 8; ++e) v[e] = rnd<T>(v[e]);
       if (CONV && a.terminal == TERM_GAP) {
-        // Sum this lane's 8 positions into the slot of their image (the tile
-        // covers at most two images), then over the lanes sharing the row.
-        const int64_t img0 = (n0 < a.N ? n0 : a.N - 1) / PQ;
-        const bool second = row_ok && valid > 0 && img != img0;
+        // This lane's positions into the slot of their image, then over the
+        // lanes sharing the row.
         const int kind = a.pool;
-        float s0 = pool_id(kind), s1 = pool_id(kind);
+        float t = pool_id(kind);
+        if (kind == MK_OP_GMP) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (e < valid) {
-            const float c = pool_in(kind, a.pool_p, v[e]);
-            if (second) s1 = pool_comb(kind, s1, c);
-            else s0 = pool_comb(kind, s0, c);
-          }
+          for (int e = 0; e < 8; ++e) t = fmaxf(t, e < valid ? v[e] : -INFINITY);
+        } else if (kind == MK_OP_LPPOOL) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) t += e < valid ? powf(v[e], a.pool_p) : 0.f;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) t += e < valid ? v[e] : 0.f;
+        }
+        float s0 = second ? pool_id(kind) : t, s1 = second ? t : pool_id(kind);
 #pragma unroll
         for (int o = LPR / 2; o > 0; o >>= 1) {
           s0 = pool_comb(kind, s0, __shfl_xor(s0, o, 64));
@@ -496,11 +496,20 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         }
       }
       if (a.terminal == TERM_LAYERNORM) {
-        // moments of this wave's columns of the row (values as stored)
-        Moments mo{0.f, 0.f, 0.f};
+        // moments of this wave's columns of the row: mean, then the squared
+        // deviations, over the lane's valid values; lanes then merge
+        float sv = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (e < valid) mom_add(mo, v[e]);
+        for (int e = 0; e < 8; ++e) sv += e < valid ? v[e] : 0.f;
+        const float n = (float)max(valid, 0);
+        const float mean = valid > 0 ? sv / n : 0.f;
+        float m2 = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float d = v[e] - mean;
+          m2 += e < valid ? d * d : 0.f;
+        }
+        Moments mo{n, mean, m2};
 #pragma unroll
         for (int o = LPR / 2; o > 0; o >>= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
         if (q == 0) {
@@ -509,15 +518,21 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         }
       } else if (a.terminal != TERM_NONE) {
         // reduce over the LPR lanes that share this row (this wave's columns)
+        float m = -INFINITY, sum = 0.f;
         if (softmax) {
 #pragma unroll
-          for (int o = LPR / 2; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-          sum = 0.f;
-          if (m != -INFINITY) {
+          for (int e = 0; e < 8; ++e) m = fmaxf(m, e < valid ? v[e] : -INFINITY);
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (e < valid) sum += __expf(v[e] - m);
+          for (int o = LPR / 2; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+          const bool any = m != -INFINITY;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float x = __expf(v[e] - m);
+            sum += (e < valid && any) ? x : 0.f;
           }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) sum += e < valid ? v[e] : 0.f;
         }
 #pragma unroll
         for (int o = LPR / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
