@@ -325,7 +325,11 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   // Per half slice and wave: MFMAs issued and fragment-read pairs.
   constexpr int kMfmaHalf = 4 * NJ * (sizeof(T) == 2 ? 1 : 4);
   constexpr int kReadPairs = (4 + NJ) / 2;
-  static_assert(PIPE != 2 || kMfmaHalf >= kReadPairs + LPS, "interleave needs more MFMAs");
+  // slice loads after the read pairs: kVm per MFMA, in kVmGroups groups
+  constexpr int kFree = kMfmaHalf - kReadPairs;
+  constexpr int kVm = kFree > 0 ? (LPS + kFree - 1) / kFree : LPS;
+  constexpr int kVmGroups = (LPS + kVm - 1) / kVm;
+  static_assert(PIPE != 2 || kMfmaHalf >= kReadPairs + kVmGroups, "interleave needs more MFMAs");
   if (PIPE) {
     // Fragment reads run one half-step (k16) ahead of the MFMAs, so the
     // barrier sits between the two halves of a slice: the MFMAs of half 0 of
@@ -369,11 +373,11 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
       }
 #pragma unroll
-      for (int g = 0; g < LPS; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+      for (int g = 0; g < kVmGroups; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, kVm, 0);   // VMEM read
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaHalf - kReadPairs - LPS, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaHalf - kReadPairs - kVmGroups, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     load_frags<NJ, T>(smem + ((nk - 1) % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
