@@ -222,3 +222,18 @@ def test_swap_keeps_workspace_and_reports_impl():
     assert m.workspace_size() == ws
     assert m.subkernels()[0]["scratch_bytes"] <= ws
     assert m.subkernels()[0]["n_launches"] == 2
+
+
+def test_empty_dimensions_are_rejected_by_both_sides():
+    """A zero-sized dimension is an error (MK_E_SHAPE) in the library and in
+    the oracle alike; there is no empty launch to take."""
+    for M in (0,):
+        m = workloads.linear_relu_rowsum(M=M, K=8, N=8)
+        with pytest.raises(mk.MkError) as e:
+            mk.mk_module_create(m, [0, 0, 0, 0])
+        assert e.value.status == 2            # MK_E_SHAPE
+        with pytest.raises(ValueError):
+            oracle.plan(m, [0, 0, 0, 0])
+    m = workloads.conv_relu_gap(N=1, C=4, H=0, W=5, K=3)
+    with pytest.raises(mk.MkError):
+        mk.mk_module_create(m, [0, 0, 0, 0])
