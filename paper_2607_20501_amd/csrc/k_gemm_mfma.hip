@@ -1,4 +1,4 @@
-// bf16 GEMM with fused epilogue on gfx950 matrix cores.
+// bf16 / fp32 GEMM with fused epilogue on gfx950 matrix cores.
 //
 //   C[z][m, n] = chain(alpha * sum_k A[z][m, k] B[z](k, n))     (fp32 accumulate)
 //
@@ -6,35 +6,43 @@
 // product (MKEvolve App. H.2 linear kernels; the fusion guidance of App. I.1:
 // GEMM followed by bias, activations, scaling and the residual add in one
 // kernel, never materialising the intermediate).  A terminal row reduction
-// that needs a full row (softmax, row-sum) is split at the column tile: the
-// epilogue emits per-(row, tile) partials and a finisher combines them
-// (App. I.1: "may need split at softmax due to reduction").
+// that needs a full row (softmax, row-sum, post-LN LayerNorm) is split at the
+// column tile: the epilogue emits per-(row, tile) partials and a finisher
+// combines them (App. I.1: "may need split at softmax due to reduction").
 //
 // Design for CDNA4:
-//  * Plain GEMMs: a 256 x 256 output tile per workgroup, K in 32-deep
-//    slices, eight waves (two per SIMD) in a 2 x 4 arrangement, each owning
-//    128 x 64 = 4 x 2 tiles of v_mfma_f32_32x32x16_bf16 (128 fp32
-//    accumulators per lane).  Conv GEMMs: 256 x 128 tiles, four waves, two
+//  * Plain GEMMs: a 256 x 256 output tile per workgroup, eight waves (two per
+//    SIMD) in a 2 x 4 arrangement, each owning 128 x 64 = 4 x 2 tiles of
+//    v_mfma_f32_32x32x16_bf16 (fp32: v_mfma_f32_32x32x2_f32), 128 fp32
+//    accumulators per lane.  Conv GEMMs: 256 x 128 tiles, four waves, two
 //    workgroups per CU.
-//  * Operands move HBM -> LDS with buffer_load ... lds (no register staging)
-//    into a ring of 32 KB slices (4 stages; 3 for conv) with one barrier per
-//    slice.  Out-of-range lanes read zeros through the buffer descriptor's
-//    range check (ragged M / N / K).
-//  * Plain GEMMs read MFMA fragments one 16-deep half-slice ahead of the
-//    MFMAs that use them, with the barrier between the two halves, so the
-//    matrix cores are fed across the barrier.
-//  * LDS rows are 64 bytes (four 16-byte chunks); chunk c of row r sits at
-//    chunk c ^ (((r >> 1) ^ (r >> 3)) & 3), so the lanes served together by a
-//    128-bit fragment read hit distinct banks.  Each lane's global address is
-//    chosen so that the lane-ordered LDS write lands in that swizzled layout.
+//  * Operands move HBM -> LDS with buffer_load ... lds (no register staging).
+//    An LDS row holds one K stage of one operand row: 128 bytes for plain
+//    GEMMs (64 bf16 / 32 fp32; eight 16-byte chunks), so every 8 lanes of a
+//    load read one whole 128-byte line and the L2 sees 128-byte requests
+//    (64-byte rows issue twice the requests and the operand stream, not the
+//    matrix cores, bounds the loop).  Conv GEMMs keep 64-byte rows (a slice
+//    must not cross a filter tap at C = 128 bf16 ... and two workgroups fit).
+//    Out-of-range lanes read zeros through the buffer descriptor's range
+//    check (ragged M / N / K).
+//  * Plain GEMMs double-buffer two 64 KB stages; within a stage the MFMA
+//    fragments are read one 16-deep sub-step ahead of the MFMAs that use them,
+//    and the one barrier per stage sits before its last sub-step, where the
+//    next stage is known landed and the freed slot is refilled.
+//  * LDS chunk c of row r sits at chunk c ^ swz(r), so the lanes served together
+//    by a 128-bit fragment read hit distinct banks; each lane's global address
+//    is chosen so that the lane-ordered LDS write lands in that layout.
 //  * MFMA operands must be K-contiguous; a weight given as [K, N] is first
 //    transposed to [N, K] in scratch by a tiled transpose launch.
 //  * Tiles are remapped so that consecutive workgroups of one XCD (the
 //    hardware deals workgroups round-robin over the 8 XCDs) take a compact
 //    group of tiles and share operand slices in that XCD's L2.
-//  * The epilogue stages 32-row slabs of accumulators through LDS so each
+//  * The epilogue stages 16-row slabs of accumulators through LDS so each
 //    lane finishes 8 consecutive columns and writes them with one 16-byte
 //    store.
+
+#include <algorithm>
+#include <type_traits>
 
 #include "dev.hpp"
 
@@ -46,34 +54,38 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 namespace {
 
-// A K slice is 64 bytes of every operand row: 32 bf16 or 16 fp32 values,
-// four 16-byte chunks.  MfmaType<T> gives the slice depth and the fragment.
+// MfmaType<T>: the MFMA fragment (one 16-byte chunk: 8 bf16 / 4 fp32
+// consecutive k of one row / column).
 template <typename T>
 struct MfmaType;
 template <>
 struct MfmaType<bf16> {
-  static constexpr int BK = 32;
-  typedef bf16x8 frag;      // 8 consecutive k of one row / column
+  typedef bf16x8 frag;
 };
 template <>
 struct MfmaType<float> {
-  static constexpr int BK = 16;
-  typedef f32x4 frag;       // 4 consecutive k
+  typedef f32x4 frag;
 };
 
 constexpr int BM = 256;
-constexpr int kRowBytes = 64;                     // one K slice of one row
-constexpr int kTileBytes = BM * kRowBytes;        // 16 KB A slice
 constexpr int kGroupM = 8;                        // tile rows per locality group
 constexpr int kXcds = 8;
 
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+// Chunk swizzles: 64-byte rows (4 chunks) and 128-byte rows (8 chunks); the 8
+// consecutive rows read together by a 128-bit fragment read map to distinct
+// physical chunks.
+template <int RB>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (RB == 64)
+    return ((r >> 1) ^ (r >> 3)) & 3;
+  else
+    return (r ^ (r >> 3)) & 7;
+}
 
-// Byte offset of chunk c of row r inside a [rows][32] bf16 operand slice.
-__device__ __forceinline__ int lds_off(int r, int c) { return r * 64 + ((c ^ swz(r)) << 4); }
-
-__device__ __forceinline__ uint32_t dw(const uint4& v, int d) {
-  return d == 0 ? v.x : d == 1 ? v.y : d == 2 ? v.z : v.w;
+// Byte offset of logical chunk c of row r in an operand stage of RB-byte rows.
+template <int RB>
+__device__ __forceinline__ int lds_off(int r, int c) {
+  return r * RB + ((c ^ swz<RB>(r)) << 4);
 }
 
 struct TileCoord {
@@ -103,35 +115,40 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
                                            0x00020000);
 }
 
-__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0));
-}
-
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Direct HBM -> LDS loads of one operand slice (ROWS x 32 bf16 = ROWS*4
-// 16-byte chunks).  For
-// load q of wave w, lane i fills LDS chunk p = (q*WAVES + w)*64 + i, i.e. row
-// p/4, physical chunk p%4, whose logical chunk is (p%4) ^ swz(row).
-template <int WAVES, int ROWS, typename T>
+// Direct HBM -> LDS loads of one operand stage (ROWS rows of RB bytes, CPR =
+// RB/16 chunks per row).  LDS chunk p of the stage is row p/CPR, physical
+// chunk p%CPR, whose logical chunk is (p%CPR) ^ swz(row): the CPR lanes of a
+// row read one contiguous RB-byte piece of it in a permuted order.
+template <int WAVES, int ROWS, typename T, int RB>
 struct SliceLoader {
-  static constexpr int E = 16 / (int)sizeof(T);        // elements per chunk
-  static constexpr int LQ = ROWS * 4 / (64 * WAVES);   // loads per thread per slice
+  static constexpr int E = 16 / (int)sizeof(T);          // elements per chunk
+  static constexpr int CPR = RB / 16;                    // chunks per row
+  static constexpr int LQ = ROWS * CPR / (64 * WAVES);   // loads per thread per stage
+  static_assert(LQ * 64 * WAVES == ROWS * CPR, "stage must split evenly over the loads");
+  // A lane's successive loads are 64*WAVES/CPR rows apart, a multiple of 64,
+  // which leaves both swizzles unchanged: one logical chunk serves them all.
+  static_assert((64 * WAVES / CPR) % 64 == 0, "swizzle must repeat across a lane's loads");
   __amdgpu_buffer_rsrc_t src;
   uint32_t voff[LQ];   // byte offset at k0 = 0, kOob if the row is out of range
-  int lchunk[LQ];      // logical 16-byte chunk of this lane's loads
+  int lchunk;          // logical 16-byte chunk of this lane's loads
+
+  __device__ __forceinline__ int first_row() const {
+    return ((threadIdx.x >> 6) * 64 + (threadIdx.x & 63)) / CPR;
+  }
+  __device__ __forceinline__ void set_chunk() {
+    const int p = (threadIdx.x >> 6) * 64 + (threadIdx.x & 63);
+    lchunk = (p % CPR) ^ swz<RB>(p / CPR);
+  }
 
   __device__ __forceinline__ void init(const T* base, int64_t rows, int64_t ld, int64_t r0) {
     src = make_rsrc(base, rows * ld * (int64_t)sizeof(T));
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    set_chunk();
 #pragma unroll
     for (int q = 0; q < LQ; ++q) {
-      const int p = (q * WAVES + w) * 64 + lane;
-      const int row = p >> 2;
-      const int c = (p & 3) ^ swz(row);
-      lchunk[q] = c;
-      const int64_t g = r0 + row;
-      voff[q] = g < rows ? (uint32_t)(g * ld * (int64_t)sizeof(T) + c * 16) : kOob;
+      const int64_t g = r0 + first_row() + q * (64 * WAVES / CPR);
+      voff[q] = g < rows ? (uint32_t)(g * ld * (int64_t)sizeof(T) + lchunk * 16) : kOob;
     }
   }
 
@@ -141,55 +158,62 @@ struct SliceLoader {
   __device__ __forceinline__ void init_gather(const T* base, int64_t bytes, int64_t rows,
                                               int64_t r0, RowOff rowoff) {
     src = make_rsrc(base, bytes);
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    set_chunk();
 #pragma unroll
     for (int q = 0; q < LQ; ++q) {
-      const int p = (q * WAVES + w) * 64 + lane;
-      const int row = p >> 2;
-      const int c = (p & 3) ^ swz(row);
-      lchunk[q] = c;
-      const int64_t g = r0 + row;
-      voff[q] = g < rows ? (uint32_t)(rowoff(g) + c * 16) : kOob;
+      const int64_t g = r0 + first_row() + q * (64 * WAVES / CPR);
+      voff[q] = g < rows ? (uint32_t)(rowoff(g) + lchunk * 16) : kOob;
     }
   }
 
-  // Issue the loads of the slice starting at k0 into `dst` (this operand's
-  // slice inside a stage); `soff` is the slice's byte offset along K.
+  // Issue the loads of the stage starting at k0 into `dst` (this operand's
+  // part of a stage); `soff` is the stage's byte offset along K.  For load q
+  // of wave w, lane i fills LDS chunk p = (q*WAVES + w)*64 + i, i.e. row
+  // p/CPR, physical chunk p%CPR.
   __device__ __forceinline__ void issue(char* dst, int64_t k0, int64_t K, uint32_t soff) const {
     const int w = threadIdx.x >> 6;
-    const int64_t krem = K - k0;
+    const bool in_k = lchunk * E < K - k0;
 #pragma unroll
-    for (int q = 0; q < LQ; ++q) {
-      const uint32_t off = lchunk[q] * E < krem ? voff[q] : kOob;
+    for (int q = 0; q < LQ; ++q)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * WAVES + w) * 1024),
-                                               16, (int)off, (int)soff, 0, 0);
-    }
+                                               16, (int)(in_k ? voff[q] : kOob), (int)soff, 0,
+                                               0);
   }
   __device__ __forceinline__ void issue(char* dst, int64_t k0, int64_t K) const {
     issue(dst, k0, K, (uint32_t)(k0 * (int64_t)sizeof(T)));
   }
+  // Loads Q0 .. Q1-1 of the stage (plain rows): a stage's loads may be spread.
+  template <int Q0, int Q1>
+  __device__ __forceinline__ void issue_part(char* dst, int64_t k0, int64_t K) const {
+    const int w = threadIdx.x >> 6;
+    const bool in_k = lchunk * E < K - k0;
+    const uint32_t soff = (uint32_t)(k0 * (int64_t)sizeof(T));
+#pragma unroll
+    for (int q = Q0; q < Q1; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * WAVES + w) * 1024),
+                                               16, (int)(in_k ? voff[q] : kOob), (int)soff, 0,
+                                               0);
+  }
 };
 
-// MFMA operand fragments of one half slice (chunks 2kk, 2kk+1) for this
-// wave: 4 row tiles of A and NJ column tiles of B; lane (lr, lh) holds the
-// 16-byte chunk 2kk+lh of row / column lr of each tile.
+// MFMA operand fragments of one sub-step (chunks 2kk, 2kk+1) for this wave:
+// 4 row tiles of A and NJ column tiles of B; lane (lr, lh) holds the 16-byte
+// chunk 2kk+lh of row / column lr of each tile.
 template <int NJ, typename T>
 struct Frags {
   typename MfmaType<T>::frag a[4], b[NJ];
 };
 
-template <int NJ, typename T>
-__device__ __forceinline__ void load_frags(const char* stage, int kk, int rowbase, int colbase,
-                                           int lr, int lh, Frags<NJ, T>& f) {
+template <int NJ, typename T, int RB>
+__device__ __forceinline__ void load_frags(const char* la, const char* lb, int kk, int rowbase,
+                                           int colbase, int lr, int lh, Frags<NJ, T>& f) {
   typedef typename MfmaType<T>::frag F;
-  const char* la = stage;
-  const char* lb = stage + kTileBytes;   // B slice follows the 256-row A slice
 #pragma unroll
   for (int i = 0; i < 4; ++i)
-    f.a[i] = *(const F*)(la + lds_off(rowbase + i * 32 + lr, kk * 2 + lh));
+    f.a[i] = *(const F*)(la + lds_off<RB>(rowbase + i * 32 + lr, kk * 2 + lh));
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
-    f.b[j] = *(const F*)(lb + lds_off(colbase + j * 32 + lr, kk * 2 + lh));
+    f.b[j] = *(const F*)(lb + lds_off<RB>(colbase + j * 32 + lr, kk * 2 + lh));
 }
 
 // bf16: one 32x32x16 MFMA per tile pair (the lane's 8 k values are the
@@ -218,21 +242,20 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
 }
 
-// Copy acc[I][j][r] (rows I*32 .. I*32+31 of this wave's tile) into the wave's
-// slab: element (row (r/4)*8 + lh*4 + r%4, column j*32 + lr), row stride LD.
-template <int I, int NJ, int LD>
-__device__ __forceinline__ void stage_slab(const f32x16 (&acc)[4][NJ], float* slab, int lh,
+// Copy rows H*16 .. H*16+15 of acc[I] (rows I*32 .. I*32+31 of this wave's
+// tile) into the wave's half slab: acc[I][j][r] with r in [8H, 8H+8) is the
+// element (row ((r/4)%2)*8 + lh*4 + r%4, column j*32 + lr), row stride LD.
+template <int I, int H, int NJ, int LD>
+__device__ __forceinline__ void stage_half(const f32x16 (&acc)[4][NJ], float* slab, int lh,
                                            int lr) {
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      slab[((r >> 2) * 8 + lh * 4 + (r & 3)) * LD + j * 32 + lr] = acc[I][j][r];
+    for (int r = 8 * H; r < 8 * H + 8; ++r)
+      slab[(((r >> 2) & 1) * 8 + lh * 4 + (r & 3)) * LD + j * 32 + lr] = acc[I][j][r];
 }
 
 // B is [N, K] (K contiguous) here; a [K, N] weight arrives pre-transposed.
-// WN waves along N (2: four waves of 128 x 128; 4: eight waves of 128 x 64,
-// two per SIMD so one wave's MFMAs cover the other's waits).
 // Byte offset along K of implicit-GEMM slice k0 (k = (r*S + s)*C + c, and a
 // slice never crosses an (r, s) boundary since C is a multiple of its depth).
 template <typename T>
@@ -242,25 +265,52 @@ __device__ __forceinline__ uint32_t conv_koff(const GemmArgs& a, int64_t k0) {
   return (uint32_t)(((r * a.cv_Wp + s) * a.cv_C + c0) * (int64_t)sizeof(T));
 }
 
+// LDS bytes of the epilogue: per wave a 16-row slab of WTN (+8) floats, then
+// the row-reduction exchange [WN][256 rows][2] floats.
+template <int WN, int BN>
+constexpr int epi_bytes() {
+  return 2 * WN * 16 * (BN / WN + 8) * 4 + WN * BM * 2 * 4;
+}
+
 // Variants: WN waves along N (2 rows of waves), BN columns per tile, STG
-// ring stages.  <4, 256, 4>: eight waves share one 256 x 256 tile (one
-// workgroup per CU).  <2, 128, 3>: four waves on a 256 x 128 tile in 72 KB of
-// LDS, so two independent workgroups share each CU.
-template <typename T, int WN, int BN, int STG, int CONV, int PIPE>
+// stages of RB-byte LDS rows, PIPE main-loop form.
+//  <4, 256, 2, 0, 2, 128>: eight waves share one 256 x 256 tile (one
+//    workgroup per CU); the stages live in five 32 KB slots, three for A and
+//    two for B ([A0 | B0 | A1 | A2 | B1]), so the A loads of a stage can be
+//    spread over the stage two ahead of it.  The workgroup is persistent: it
+//    walks the tiles v = blockIdx.x, blockIdx.x + gridDim.x, ..., and issues
+//    the next tile's stage 0 and the A part of its stage 1 before the
+//    epilogue of the current one, so the epilogue's stores drain while they
+//    arrive (the epilogue's LDS region is slots A2 and B1).
+//  <2, 128, 3, 1, 0, 64> (conv): four waves on a 256 x 128 tile in 72 KB of
+//    LDS, so two independent workgroups share each CU; one tile per workgroup.
+template <typename T, int WN, int BN, int STG, int CONV, int PIPE, int RB>
 __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kernel(GemmArgs a) {
-  constexpr int BK = MfmaType<T>::BK;
+  constexpr int BK = RB / (int)sizeof(T);   // K depth of a stage
+  constexpr int KSUB = RB / 32;             // 16-byte chunk pairs (MFMA sub-steps) per stage
   constexpr int WAVES = 2 * WN, THREADS = 64 * WAVES;
   constexpr int kStages = STG;
-  constexpr int kStageBytes = (BM + BN) * kRowBytes;
+  constexpr int kABytes = BM * RB;          // A part of a stage
+  constexpr int kBBytes = BN * RB;          // B part of a stage
+  constexpr int kStageBytes = kABytes + kBBytes;
   constexpr int WTN = BN / WN;        // wave tile columns
   constexpr int NJ = WTN / 32;        // 32-wide column tiles per wave
   constexpr int LD = WTN + 8;         // epilogue slab row stride (floats)
   constexpr int LPR = WTN / 8;        // lanes per slab row in the epilogue
   constexpr int RPP = 64 / LPR;       // slab rows per pass
-  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStageBytes];
+  constexpr bool kPersist = !CONV && PIPE != 0;
+  static_assert(PIPE == 0 || (KSUB == 4 && kABytes == 32768 && kBBytes == 32768),
+                "the pipelined loop is k64 stages of a 256 x 256 tile");
+  // Pipelined slots: A0 0, B0 32K, A1 64K, A2 96K, B1 128K; the epilogue
+  // uses A2 + B1.  Ring form: stage slots back to back, epilogue at 0.
+  constexpr int kEpiOff = kPersist ? 3 * 32768 : 0;
+  constexpr int kEpiEnd = kEpiOff + epi_bytes<WN, BN>();
+  constexpr int kRing = PIPE ? 5 * 32768 : kStages * kStageBytes;
+  constexpr int kSmem = kEpiEnd > kRing ? kEpiEnd : kRing;
+  static_assert(kSmem <= 163840, "LDS is 160 KB");
+  __shared__ __attribute__((aligned(1024))) char smem[kSmem];
   const int tiles_m = (int)((a.M + BM - 1) / BM), tiles_n = (int)((a.N + BN - 1) / BN);
-  const TileCoord tc = tile_of(blockIdx.x, tiles_m, tiles_n);
-  const int64_t m0 = (int64_t)tc.tm * BM, n0 = (int64_t)tc.tn * BN;
+  const int tiles = tiles_m * tiles_n;
   const int64_t z = blockIdx.y, bb = z / a.heads, hh = z % a.heads;
   const T* A = (const T*)a.A + a.a_off + bb * a.a_sb + hh * a.a_sh;
   const T* B = (const T*)a.B + a.b_off + bb * a.b_sb + hh * a.b_sh;
@@ -269,49 +319,70 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   const int wm = w / WN, wn = w % WN;
   const int lr = lane & 31, lh = lane >> 5;
   const int rowbase = wm * 128, colbase = wn * WTN;
-
-  f32x16 acc[4][NJ];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
   const int nk = (int)((a.K + BK - 1) / BK);
-  SliceLoader<WAVES, BM, T> la;
-  SliceLoader<WAVES, BN, T> lb;
-  la.init(A, a.M, a.lda, m0);
   const int64_t PQ = a.cv_P * a.cv_Q;
-  if (CONV) {
-    const int64_t bytes = a.cv_Hp * a.cv_Wp * a.cv_C * (int64_t)sizeof(T) * (a.N / PQ);
-    lb.init_gather(B, bytes, a.N, n0, [&](int64_t m) {
-      const int64_t n = m / PQ, pq = m % PQ;
-      const int64_t p = pq / a.cv_Q, q = pq % a.cv_Q;
-      return ((n * a.cv_Hp + p * a.cv_stride) * a.cv_Wp + q * a.cv_stride) * a.cv_C *
-             (int64_t)sizeof(T);
-    });
-  } else {
-    lb.init(B, a.N, a.ldb, n0);
-  }
-  auto issue_b = [&](char* dst, int64_t k0) {
-    if (CONV)
-      lb.issue(dst, k0, a.K, conv_koff<T>(a, k0));
-    else
-      lb.issue(dst, k0, a.K);
-  };
-  // The pipelined form issues all kStages - 1 leading slices even when K has
-  // fewer (the surplus ones read zeros), so its wait counts are exact.
-#pragma unroll
-  for (int s = 0; s < kStages - 1; ++s)
-    if (PIPE || s < nk) {
-      la.issue(smem + s * kStageBytes, (int64_t)s * BK, a.K);
-      issue_b(smem + s * kStageBytes + kTileBytes, (int64_t)s * BK);
-    }
 
-  constexpr int LPS = SliceLoader<WAVES, BM, T>::LQ + SliceLoader<WAVES, BN, T>::LQ;
-  // Wait until at most `later` slices issued after the one needed are still
-  // in flight (each slice is LPS loads of this wave, issued in order).
+  SliceLoader<WAVES, BM, T, RB> la;
+  SliceLoader<WAVES, BN, T, RB> lb;
+  auto init_loaders = [&](const TileCoord& t) {
+    const int64_t m0 = (int64_t)t.tm * BM, n0 = (int64_t)t.tn * BN;
+    la.init(A, a.M, a.lda, m0);
+    if (CONV) {
+      const int64_t bytes = a.cv_Hp * a.cv_Wp * a.cv_C * (int64_t)sizeof(T) * (a.N / PQ);
+      lb.init_gather(B, bytes, a.N, n0, [&](int64_t m) {
+        const int64_t n = m / PQ, pq = m % PQ;
+        const int64_t p = pq / a.cv_Q, q = pq % a.cv_Q;
+        return ((n * a.cv_Hp + p * a.cv_stride) * a.cv_Wp + q * a.cv_stride) * a.cv_C *
+               (int64_t)sizeof(T);
+      });
+    } else {
+      lb.init(B, a.N, a.ldb, n0);
+    }
+  };
+  // Slot addresses.  Pipelined: A of stage ks in A slot ks % 3, B in B slot
+  // ks % 2.  Ring: stage ks in slot ks % STG (A part, then B part).
+  auto a_slot = [&](int ks) -> char* {
+    if (PIPE) {
+      const int i = ks % 3;
+      return smem + (i == 0 ? 0 : i == 1 ? 65536 : 98304);
+    }
+    return smem + (ks % kStages) * kStageBytes;
+  };
+  auto b_slot = [&](int ks) -> char* {
+    if (PIPE) return smem + ((ks & 1) ? 131072 : 32768);
+    return smem + (ks % kStages) * kStageBytes + kABytes;
+  };
+  // Loads of stage ks (stages past the last read zeros: every lane's K bound
+  // fails).
+  auto issue_a = [&](int ks) { la.issue(a_slot(ks), (int64_t)ks * BK, a.K); };
+  auto issue_b = [&](int ks) {
+    const int64_t k0 = (int64_t)ks * BK;
+    if (CONV)
+      lb.issue(b_slot(ks), k0, a.K, conv_koff<T>(a, k0));
+    else
+      lb.issue(b_slot(ks), k0, a.K);
+  };
+
+  int v = blockIdx.x;
+  TileCoord tc = tile_of(v, tiles_m, tiles_n);
+  init_loaders(tc);
+  if (PIPE) {
+    issue_a(0);
+    issue_b(0);
+    issue_a(1);
+  } else {
+#pragma unroll
+    for (int s = 0; s < kStages - 1; ++s)
+      if (s < nk) {
+        issue_a(s);
+        issue_b(s);
+      }
+  }
+
+  constexpr int LA = SliceLoader<WAVES, BM, T, RB>::LQ, LB = SliceLoader<WAVES, BN, T, RB>::LQ;
+  constexpr int LPS = LA + LB;
+  // Wait until at most `later` stages issued after the one needed are still
+  // in flight (each stage is LPS loads of this wave, issued in order).
   auto wait_slices = [](int later) {
     if (later >= 3)
       wait_vm<3 * LPS>();
@@ -322,291 +393,345 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     else
       wait_vm<0>();
   };
-  // Per half slice and wave: MFMAs issued and fragment-read pairs.
-  constexpr int kMfmaHalf = 4 * NJ * (sizeof(T) == 2 ? 1 : 4);
+  // Per sub-step and wave: MFMAs issued and fragment-read pairs.
+  constexpr int kMfmaSub = 4 * NJ * (sizeof(T) == 2 ? 1 : 4);
   constexpr int kReadPairs = (4 + NJ) / 2;
-  // slice loads after the read pairs: kVm per MFMA, in kVmGroups groups
-  constexpr int kFree = kMfmaHalf - kReadPairs;
-  constexpr int kVm = kFree > 0 ? (LPS + kFree - 1) / kFree : LPS;
-  constexpr int kVmGroups = (LPS + kVm - 1) / kVm;
-  static_assert(PIPE != 2 || kMfmaHalf >= kReadPairs + kVmGroups, "interleave needs more MFMAs");
-  if (PIPE) {
-    // Fragment reads run one half-step (k16) ahead of the MFMAs, so the
-    // barrier sits between the two halves of a slice: the MFMAs of half 0 of
-    // slice kt overlap the reads of its half 1, those of half 1 the reads of
-    // half 0 of slice kt+1.  At the barrier of step kt every wave has
-    // consumed slice kt-1 (its half-1 MFMAs waited on those reads), so that
-    // slot takes slice kt+STG-1.
-    wait_vm<(kStages - 2) * LPS>();
-    __builtin_amdgcn_s_barrier();
-    Frags<NJ, T> f0, f1;
-    load_frags<NJ, T>(smem, 0, rowbase, colbase, lr, lh, f0);
-    // Branch-free body: the refill is issued every step; past the last
-    // slice every lane's offset is out of the descriptor's range, so it
-    // only writes zeros into the slot just consumed, which is never read
-    // again.  Exactly kStages - 3 slices are then in flight after the one
-    // needed, and the scheduler can spread the reads and loads between the
-    // MFMAs (one MFMA, then two reads, ...).
-    for (int kt = 0; kt < nk - 1; ++kt) {
-      load_frags<NJ, T>(smem + (kt % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
-      mfma_step<NJ, T>(f0, acc);
-#pragma unroll
-      for (int g = 0; g < kReadPairs; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaHalf - kReadPairs, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      wait_vm<(kStages - 3) * LPS>();
-      __builtin_amdgcn_s_barrier();
-      __builtin_amdgcn_sched_barrier(0);
-      const int nxt = kt + kStages - 1;
-      char* st = smem + (nxt % kStages) * kStageBytes;
-      load_frags<NJ, T>(smem + ((kt + 1) % kStages) * kStageBytes, 0, rowbase, colbase, lr, lh,
-                        f0);
-      la.issue(st, (int64_t)nxt * BK, a.K);
-      issue_b(st + kTileBytes, (int64_t)nxt * BK);
-      mfma_step<NJ, T>(f1, acc);
-#pragma unroll
-      for (int g = 0; g < kReadPairs; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
-      }
-#pragma unroll
-      for (int g = 0; g < kVmGroups; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x020, kVm, 0);   // VMEM read
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, kMfmaHalf - kReadPairs - kVmGroups, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    load_frags<NJ, T>(smem + ((nk - 1) % kStages) * kStageBytes, 1, rowbase, colbase, lr, lh, f1);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step<NJ, T>(f0, acc);
-    mfma_step<NJ, T>(f1, acc);
-  } else {
-    for (int kt = 0; kt < nk; ++kt) {
-      // Slice kt has landed once at most the loads of the later slices are
-      // outstanding.
-      wait_slices(min(kStages - 2, nk - 1 - kt));
-      // A bare barrier: __syncthreads() would also drain every outstanding
-      // load (its fence), which defeats the ring.  The slice's own loads are
-      // complete (vmcnt above), and fragment reads of the slot about to be
-      // refilled were consumed by MFMAs before this point.
-      __builtin_amdgcn_s_barrier();
-      const int nxt = kt + kStages - 1;
-      if (nxt < nk) {
-        char* st = smem + (nxt % kStages) * kStageBytes;
-        la.issue(st, (int64_t)nxt * BK, a.K);
-        issue_b(st + kTileBytes, (int64_t)nxt * BK);
-      }
-      const char* cur = smem + (kt % kStages) * kStageBytes;
-      Frags<NJ, T> f0, f1;
-      load_frags<NJ, T>(cur, 0, rowbase, colbase, lr, lh, f0);
-      load_frags<NJ, T>(cur, 1, rowbase, colbase, lr, lh, f1);
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step<NJ, T>(f0, acc);
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step<NJ, T>(f1, acc);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  }
+  // A loads: half in sub-step 0, half in sub-step 1; B loads in sub-step 3.
+  constexpr int kA0 = (LA + 1) / 2, kA1 = LA - kA0;
+  static_assert(PIPE == 0 || kMfmaSub >= kReadPairs + LB + 1, "interleave needs more MFMAs");
 
-  // ---------------------------------------------------------------- epilogue
-  // acc[i][j][r] is C[row, col] with
-  //   row = m0 + rowbase + i*32 + (r/4)*8 + lh*4 + r%4,  col = n0 + colbase + j*32 + lr.
-  // Each wave stages one 32-row slab at a time in its own LDS region, then
-  // every lane applies the chain to 8 consecutive columns and writes them with
-  // one 16-byte store.
-  wait_vm<0>();
-  __syncthreads();   // operand slices are dead; reuse LDS
-  float* slab = (float*)smem + w * (32 * LD);
-  float* red = (float*)smem + WAVES * 32 * LD;   // [WN column groups][256 rows][2]
+  float* slab = (float*)(smem + kEpiOff) + w * (16 * LD);
+  float* red = (float*)(smem + kEpiOff) + WAVES * 16 * LD;   // [WN column groups][256 rows][2]
   const int64_t cbase = a.c_off + bb * a.c_sb + hh * a.c_sh;
   T* C = (T*)a.C + cbase;
   const bool softmax = a.terminal == TERM_SOFTMAX;
   const int q = lane % LPR;          // 8-column group within the slab row
-  const int64_t col0 = n0 + colbase + q * 8;
   // 16-byte accesses to C and to residual operands need 8-aligned offsets.
   const bool vec_ok = ((a.ldc | cbase) & 7) == 0;
-  const int valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
-  // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0); the tile
-  // covers at most two, and slot 1 is the second.
-  const int64_t img = CONV ? col0 / PQ : 0;
-  const bool second = CONV && valid > 0 && img != (n0 < a.N ? n0 : a.N - 1) / PQ;
 
-  auto finish_slab = [&](int i) {
-    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): slab writes done (wave-private)
-    __builtin_amdgcn_wave_barrier();
-    for (int pass = 0; pass < 32 / RPP; ++pass) {
-      const int rl = pass * RPP + lane / LPR;
-      const int lrow = rowbase + i * 32 + rl;
-      const int64_t row = m0 + lrow;
-      const float4 lo = *(const float4*)(slab + rl * LD + q * 8);
-      const float4 hi = *(const float4*)(slab + rl * LD + q * 8 + 4);
-      float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-      const bool row_ok = row < a.M;
+  for (;;) {
+    const int64_t m0 = (int64_t)tc.tm * BM, n0 = (int64_t)tc.tn * BN;
+    f32x16 acc[4][NJ];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] *= a.alpha;
-      // Offset of (row, col0) in the output: row-major, or NCHW for a conv
-      // (row = channel, col = position).
-      const int64_t obase = CONV ? (img * a.M + row) * PQ + (col0 - img * PQ)
-                                 : cbase + row * a.ldc + col0;
-      if (a.epi.n && row_ok && valid > 0)
-        epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok));
-      // Stored values are rounded to the storage type; reductions that need
-      // the whole row read them back as stored.  Below, lanes past N take
-      // part through selects, not branches.
-      if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX || a.terminal == TERM_LAYERNORM)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = rnd<T>(v[e]);
-      if (CONV && a.terminal == TERM_GAP) {
-        // This lane's positions into the slot of their image, then over the
-        // lanes sharing the row.
-        const int kind = a.pool;
-        float t = pool_id(kind);
-        if (kind == MK_OP_GMP) {
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) t = fmaxf(t, e < valid ? v[e] : -INFINITY);
-        } else if (kind == MK_OP_LPPOOL) {
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    if (PIPE) {
+      // In flight: A(0), B(0), A(1) (issued before the loop or during the
+      // previous tile's epilogue); B(1) goes now.  Stage s: sub-steps 0..3,
+      // fragments one sub-step ahead of the MFMAs that use them; A(s+2) is
+      // issued over sub-steps 0 and 1 (its slot held stage s-1, released by
+      // the barrier of stage s-1).  Before sub-step 3 the wave waits for its
+      // loads of stage s+1 (only A(s+2) may remain) and for its reads of
+      // stage s (lgkmcnt(0)); one barrier makes both hold for every wave,
+      // after which stage s+1 is read and B(s+2) refills B slot s % 2.  The
+      // body is branch-free: past the last stage every lane's K bound fails
+      // and the loads only write zeros into slots never read again.
+      issue_b(1);
+      wait_vm<LB>();
+      __builtin_amdgcn_s_barrier();
+      Frags<NJ, T> f0, f1;
+      load_frags<NJ, T, RB>(a_slot(0), b_slot(0), 0, rowbase, colbase, lr, lh, f0);
+      for (int ks = 0; ks < nk; ++ks) {
+        const char* ca = a_slot(ks);
+        const char* cb = b_slot(ks);
+        // sub-steps 0..2: MFMAs on the fragments of `sub`, reads of sub+1
+        auto sub_step = [&](auto SUB) {
+          constexpr int sub = decltype(SUB)::value;
+          Frags<NJ, T>& use = (sub & 1) ? f1 : f0;
+          Frags<NJ, T>& fill = (sub & 1) ? f0 : f1;
+          load_frags<NJ, T, RB>(ca, cb, sub + 1, rowbase, colbase, lr, lh, fill);
+          if constexpr (sub == 0)
+            la.template issue_part<0, kA0>(a_slot(ks + 2), (int64_t)(ks + 2) * BK, a.K);
+          if constexpr (sub == 1)
+            la.template issue_part<kA0, LA>(a_slot(ks + 2), (int64_t)(ks + 2) * BK, a.K);
+          mfma_step<NJ, T>(use, acc);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) t += e < valid ? powf(v[e], a.pool_p) : 0.f;
-        } else {
+          for (int g = 0; g < kReadPairs; ++g) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
+          }
+          constexpr int nv = sub == 0 ? kA0 : sub == 1 ? kA1 : 0;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) t += e < valid ? v[e] : 0.f;
+          for (int g = 0; g < nv; ++g) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, kMfmaSub - kReadPairs - nv, 0);
+          __builtin_amdgcn_sched_barrier(0);
+        };
+        sub_step(std::integral_constant<int, 0>{});
+        sub_step(std::integral_constant<int, 1>{});
+        sub_step(std::integral_constant<int, 2>{});
+        // last sub-step (fragments in f1)
+        wait_vm<LA>();
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags<NJ, T, RB>(a_slot(ks + 1), b_slot(ks + 1), 0, rowbase, colbase, lr, lh, f0);
+        issue_b(ks + 2);
+        mfma_step<NJ, T>(f1, acc);
+#pragma unroll
+        for (int g = 0; g < kReadPairs; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
         }
-        float s0 = second ? pool_id(kind) : t, s1 = second ? t : pool_id(kind);
 #pragma unroll
-        for (int o = LPR / 2; o > 0; o >>= 1) {
-          s0 = pool_comb(kind, s0, __shfl_xor(s0, o, 64));
-          s1 = pool_comb(kind, s1, __shfl_xor(s1, o, 64));
+        for (int g = 0; g < LB; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
         }
-        if (q == 0) {
-          red[(wn * 256 + lrow) * 2] = s0;
-          red[(wn * 256 + lrow) * 2 + 1] = s1;
-        }
-        continue;
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfmaSub - kReadPairs - LB, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      if (a.terminal != TERM_ROWSUM && row_ok) {
-        // NCHW conv output is always 8-aligned (PQ % 8 == 0); a row-major
-        // output needs ldc and the batch offset 8-aligned for the vector store.
-        const int64_t off = CONV ? obase : row * a.ldc + col0;
-        if (valid == 8 && (CONV || vec_ok)) {
-          st8<T>(C + off, v);
-        } else {
+    } else {
+      for (int kt = 0; kt < nk; ++kt) {
+        // Stage kt has landed once at most the loads of the later stages are
+        // outstanding.
+        wait_slices(min(kStages - 2, nk - 1 - kt));
+        // A bare barrier: __syncthreads() would also drain every outstanding
+        // load (its fence), which defeats the ring.  The stage's own loads are
+        // complete (vmcnt above), and fragment reads of the slot about to be
+        // refilled were consumed by MFMAs before this point.
+        __builtin_amdgcn_s_barrier();
+        const int nxt = kt + kStages - 1;
+        if (nxt < nk) {
+          issue_a(nxt);
+          issue_b(nxt);
+        }
+        Frags<NJ, T> f[KSUB];
 #pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (e < valid) st<T>(C, off + e, v[e]);
+        for (int sub = 0; sub < KSUB; ++sub)
+          load_frags<NJ, T, RB>(a_slot(kt), b_slot(kt), sub, rowbase, colbase, lr, lh, f[sub]);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int sub = 0; sub < KSUB; ++sub) {
+          mfma_step<NJ, T>(f[sub], acc);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
-      if (a.terminal == TERM_LAYERNORM) {
-        // moments of this wave's columns of the row: mean, then the squared
-        // deviations, over the lane's valid values; lanes then merge
-        float sv = 0.f;
+    }
+
+    // Every slot is consumed and every refill (zeros past the last stage)
+    // has landed; the next tile's A(0), B(0), A(1) go into slots A0, B0, A1,
+    // below the epilogue's region.
+    wait_vm<0>();
+    __syncthreads();
+    const int vn = v + (int)gridDim.x;
+    const bool more = kPersist && vn < tiles;
+    TileCoord tnext = tc;
+    if (more) {
+      tnext = tile_of(vn, tiles_m, tiles_n);
+      init_loaders(tnext);
+      issue_a(0);
+      issue_b(0);
+      issue_a(1);
+    }
+
+    // ---------------------------------------------------------------- epilogue
+    // acc[i][j][r] is C[row, col] with
+    //   row = m0 + rowbase + i*32 + (r/4)*8 + lh*4 + r%4,  col = n0 + colbase + j*32 + lr.
+    // Each wave stages 16 rows at a time in its own LDS region, then every
+    // lane applies the chain to 8 consecutive columns and writes them with one
+    // 16-byte store.
+    const int64_t col0 = n0 + colbase + q * 8;
+    const int valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
+    // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0); the tile
+    // covers at most two, and slot 1 is the second.
+    const int64_t img = CONV ? col0 / PQ : 0;
+    const bool second = CONV && valid > 0 && img != (n0 < a.N ? n0 : a.N - 1) / PQ;
+
+    auto finish_half = [&](int i, int h) {
+      __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): slab writes done (wave-private)
+      __builtin_amdgcn_wave_barrier();
+      for (int pass = 0; pass < 16 / RPP; ++pass) {
+        const int rl = pass * RPP + lane / LPR;
+        const int lrow = rowbase + i * 32 + h * 16 + rl;
+        const int64_t row = m0 + lrow;
+        const float4 lo = *(const float4*)(slab + rl * LD + q * 8);
+        const float4 hi = *(const float4*)(slab + rl * LD + q * 8 + 4);
+        float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        const bool row_ok = row < a.M;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sv += e < valid ? v[e] : 0.f;
-        const float n = (float)max(valid, 0);
-        const float mean = valid > 0 ? sv / n : 0.f;
-        float m2 = 0.f;
+        for (int e = 0; e < 8; ++e) v[e] *= a.alpha;
+        // Offset of (row, col0) in the output: row-major, or NCHW for a conv
+        // (row = channel, col = position).
+        const int64_t obase = CONV ? (img * a.M + row) * PQ + (col0 - img * PQ)
+                                   : cbase + row * a.ldc + col0;
+        if (a.epi.n && row_ok && valid > 0)
+          epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok));
+        // Stored values are rounded to the storage type; reductions that need
+        // the whole row read them back as stored.  Below, lanes past N take
+        // part through selects, not branches.
+        if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX || a.terminal == TERM_LAYERNORM)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float d = v[e] - mean;
-          m2 += e < valid ? d * d : 0.f;
+          for (int e = 0; e < 8; ++e) v[e] = rnd<T>(v[e]);
+        if (CONV && a.terminal == TERM_GAP) {
+          // This lane's positions into the slot of their image, then over the
+          // lanes sharing the row.
+          const int kind = a.pool;
+          float t = pool_id(kind);
+          if (kind == MK_OP_GMP) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) t = fmaxf(t, e < valid ? v[e] : -INFINITY);
+          } else if (kind == MK_OP_LPPOOL) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) t += e < valid ? powf(v[e], a.pool_p) : 0.f;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) t += e < valid ? v[e] : 0.f;
+          }
+          float s0 = second ? pool_id(kind) : t, s1 = second ? t : pool_id(kind);
+#pragma unroll
+          for (int o = LPR / 2; o > 0; o >>= 1) {
+            s0 = pool_comb(kind, s0, __shfl_xor(s0, o, 64));
+            s1 = pool_comb(kind, s1, __shfl_xor(s1, o, 64));
+          }
+          if (q == 0) {
+            red[(wn * 256 + lrow) * 2] = s0;
+            red[(wn * 256 + lrow) * 2 + 1] = s1;
+          }
+          continue;
         }
-        Moments mo{n, mean, m2};
+        if (a.terminal != TERM_ROWSUM && row_ok) {
+          // NCHW conv output is always 8-aligned (PQ % 8 == 0); a row-major
+          // output needs ldc and the batch offset 8-aligned for the vector store.
+          const int64_t off = CONV ? obase : row * a.ldc + col0;
+          if (valid == 8 && (CONV || vec_ok)) {
+            st8<T>(C + off, v);
+          } else {
 #pragma unroll
-        for (int o = LPR / 2; o > 0; o >>= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
-        if (q == 0) {
-          red[(wn * 256 + lrow) * 2] = mo.mean;
-          red[(wn * 256 + lrow) * 2 + 1] = mo.m2;
+            for (int e = 0; e < 8; ++e)
+              if (e < valid) st<T>(C, off + e, v[e]);
+          }
         }
-      } else if (a.terminal != TERM_NONE) {
-        // reduce over the LPR lanes that share this row (this wave's columns)
-        float m = -INFINITY, sum = 0.f;
-        if (softmax) {
+        if (a.terminal == TERM_LAYERNORM) {
+          // moments of this wave's columns of the row: mean, then the squared
+          // deviations, over the lane's valid values; lanes then merge
+          float sv = 0.f;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) m = fmaxf(m, e < valid ? v[e] : -INFINITY);
-#pragma unroll
-          for (int o = LPR / 2; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-          const bool any = m != -INFINITY;
+          for (int e = 0; e < 8; ++e) sv += e < valid ? v[e] : 0.f;
+          const float n = (float)max(valid, 0);
+          const float mean = valid > 0 ? sv / n : 0.f;
+          float m2 = 0.f;
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const float x = __expf(v[e] - m);
-            sum += (e < valid && any) ? x : 0.f;
+            const float d = v[e] - mean;
+            m2 += e < valid ? d * d : 0.f;
           }
+          Moments mo{n, mean, m2};
+#pragma unroll
+          for (int o = LPR / 2; o > 0; o >>= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
+          if (q == 0) {
+            red[(wn * 256 + lrow) * 2] = mo.mean;
+            red[(wn * 256 + lrow) * 2 + 1] = mo.m2;
+          }
+        } else if (a.terminal != TERM_NONE) {
+          // reduce over the LPR lanes that share this row (this wave's columns)
+          float m = -INFINITY, sum = 0.f;
+          if (softmax) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) m = fmaxf(m, e < valid ? v[e] : -INFINITY);
+#pragma unroll
+            for (int o = LPR / 2; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+            const bool any = m != -INFINITY;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float x = __expf(v[e] - m);
+              sum += (e < valid && any) ? x : 0.f;
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sum += e < valid ? v[e] : 0.f;
+          }
+#pragma unroll
+          for (int o = LPR / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
+          if (q == 0) {
+            red[(wn * 256 + lrow) * 2] = m;
+            red[(wn * 256 + lrow) * 2 + 1] = sum;
+          }
+        }
+      }
+      // The slab is rewritten next: every lane's reads of it must be done.
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_wave_barrier();
+    };
+    // A switch keeps every acc index static while the finishing code exists
+    // once (the loop itself is not unrolled).
+    for (int s = 0; s < 8; ++s) {
+      switch (s) {
+        case 0: stage_half<0, 0, NJ, LD>(acc, slab, lh, lr); break;
+        case 1: stage_half<0, 1, NJ, LD>(acc, slab, lh, lr); break;
+        case 2: stage_half<1, 0, NJ, LD>(acc, slab, lh, lr); break;
+        case 3: stage_half<1, 1, NJ, LD>(acc, slab, lh, lr); break;
+        case 4: stage_half<2, 0, NJ, LD>(acc, slab, lh, lr); break;
+        case 5: stage_half<2, 1, NJ, LD>(acc, slab, lh, lr); break;
+        case 6: stage_half<3, 0, NJ, LD>(acc, slab, lh, lr); break;
+        default: stage_half<3, 1, NJ, LD>(acc, slab, lh, lr); break;
+      }
+      finish_half(s >> 1, s & 1);
+    }
+    if (a.terminal != TERM_NONE) {
+      __syncthreads();
+      for (int lrow = threadIdx.x; lrow < BM; lrow += THREADS) {
+        const int64_t row = m0 + lrow;
+        if (row >= a.M) break;
+        if (CONV) {   // GAP partials of this position tile, per image slot
+#pragma unroll
+          for (int slot = 0; slot < 2; ++slot) {
+            float ss = pool_id(a.pool);
+#pragma unroll
+            for (int g = 0; g < WN; ++g)
+              ss = pool_comb(a.pool, ss, red[(g * 256 + lrow) * 2 + slot]);
+            a.partial[((int64_t)tc.tn * 2 + slot) * a.M + row] = ss;
+          }
+          continue;
+        }
+        float* part = a.partial + (row * a.n_tiles + tc.tn) *
+                                      (softmax || a.terminal == TERM_LAYERNORM ? 2 : 1);
+        if (a.terminal == TERM_LAYERNORM) {
+          // combine the WN waves' column ranges (their counts follow from N)
+          Moments mo{0.f, 0.f, 0.f};
+#pragma unroll
+          for (int g = 0; g < WN; ++g) {
+            const int64_t c0 = n0 + g * WTN;
+            const float cnt = (float)min<int64_t>(WTN, max<int64_t>(0, a.N - c0));
+            mo = mom_comb(mo, Moments{cnt, red[(g * 256 + lrow) * 2], red[(g * 256 + lrow) * 2 + 1]});
+          }
+          part[0] = mo.mean;
+          part[1] = mo.m2;
+        } else if (softmax) {
+          float mm = -INFINITY;
+#pragma unroll
+          for (int g = 0; g < WN; ++g) mm = fmaxf(mm, red[(g * 256 + lrow) * 2]);
+          float ss = 0.f;
+          if (mm != -INFINITY) {
+#pragma unroll
+            for (int g = 0; g < WN; ++g) {
+              const float mg = red[(g * 256 + lrow) * 2];
+              if (mg != -INFINITY) ss += red[(g * 256 + lrow) * 2 + 1] * __expf(mg - mm);
+            }
+          }
+          part[0] = mm;
+          part[1] = ss;
         } else {
+          float ss = 0.f;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) sum += e < valid ? v[e] : 0.f;
-        }
-#pragma unroll
-        for (int o = LPR / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
-        if (q == 0) {
-          red[(wn * 256 + lrow) * 2] = m;
-          red[(wn * 256 + lrow) * 2 + 1] = sum;
+          for (int g = 0; g < WN; ++g) ss += red[(g * 256 + lrow) * 2 + 1];
+          part[0] = ss;
         }
       }
     }
-    __builtin_amdgcn_wave_barrier();
-  };
-  // A switch keeps every acc index static while the finishing code exists
-  // once (the loop itself is not unrolled).
-  for (int i = 0; i < 4; ++i) {
-    switch (i) {
-      case 0: stage_slab<0, NJ, LD>(acc, slab, lh, lr); break;
-      case 1: stage_slab<1, NJ, LD>(acc, slab, lh, lr); break;
-      case 2: stage_slab<2, NJ, LD>(acc, slab, lh, lr); break;
-      default: stage_slab<3, NJ, LD>(acc, slab, lh, lr); break;
-    }
-    finish_slab(i);
-  }
-  if (a.terminal == TERM_NONE) return;
-  __syncthreads();
-  for (int lrow = threadIdx.x; lrow < BM; lrow += THREADS) {
-    const int64_t row = m0 + lrow;
-    if (row >= a.M) break;
-    if (CONV) {   // GAP partials of this position tile, per image slot
-#pragma unroll
-      for (int slot = 0; slot < 2; ++slot) {
-        float ss = pool_id(a.pool);
-#pragma unroll
-        for (int g = 0; g < WN; ++g) ss = pool_comb(a.pool, ss, red[(g * 256 + lrow) * 2 + slot]);
-        a.partial[((int64_t)tc.tn * 2 + slot) * a.M + row] = ss;
-      }
-      continue;
-    }
-    float* part = a.partial +
-                  (row * a.n_tiles + tc.tn) * (softmax || a.terminal == TERM_LAYERNORM ? 2 : 1);
-    if (a.terminal == TERM_LAYERNORM) {
-      // combine the WN waves' column ranges (their counts follow from N)
-      Moments acc{0.f, 0.f, 0.f};
-#pragma unroll
-      for (int g = 0; g < WN; ++g) {
-        const int64_t c0 = n0 + g * WTN;
-        const float cnt = (float)min<int64_t>(WTN, max<int64_t>(0, a.N - c0));
-        acc = mom_comb(acc, Moments{cnt, red[(g * 256 + lrow) * 2], red[(g * 256 + lrow) * 2 + 1]});
-      }
-      part[0] = acc.mean;
-      part[1] = acc.m2;
-    } else if (softmax) {
-      float mm = -INFINITY;
-#pragma unroll
-      for (int g = 0; g < WN; ++g) mm = fmaxf(mm, red[(g * 256 + lrow) * 2]);
-      float ss = 0.f;
-      if (mm != -INFINITY) {
-#pragma unroll
-        for (int g = 0; g < WN; ++g) {
-          const float mg = red[(g * 256 + lrow) * 2];
-          if (mg != -INFINITY) ss += red[(g * 256 + lrow) * 2 + 1] * __expf(mg - mm);
-        }
-      }
-      part[0] = mm;
-      part[1] = ss;
-    } else {
-      float ss = 0.f;
-#pragma unroll
-      for (int g = 0; g < WN; ++g) ss += red[(g * 256 + lrow) * 2 + 1];
-      part[0] = ss;
-    }
+    if (!more) break;
+    // The epilogue's LDS reads are done before any wave refills slots A2 /
+    // B1, which hold its region; red is rewritten only after that loop.
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_s_barrier();
+    v = vn;
+    tc = tnext;
   }
 }
 
@@ -691,14 +816,30 @@ GemmArgs gemm_with_bt(const GemmArgs& a, const void* bt) {
   return g;
 }
 
+// Compute units of the current device (cached per device).
+static int cu_count() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cache[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+      n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
 template <typename T>
 static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
-  // (The conv variant keeps the plain loop: with three stages the pipelined
-  // one would leave only one step of load latency hiding.)
+  // (The conv variant keeps 64-byte rows and the plain three-stage ring: two
+  // workgroups per CU, and C = 128 bf16 channels per filter tap.)
   if (a.conv)
-    hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kConvTileN, 3, 1, 0>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kConvTileN, 3, 1, 0, 64>), grid, dim3(256), 0, st,
+                       a);
   else
-    hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 4, 0, 2>), grid, dim3(512), 0, st, a);
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 2, 0, 2, 128>), grid, dim3(512), 0, st,
+                       a);
 }
 
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
@@ -714,7 +855,14 @@ hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
   if (((uintptr_t)a.A | (uintptr_t)a.B) % 16) return hipErrorInvalidValue;
   const int64_t bn = a.conv ? kConvTileN : kGemmTileN;
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + bn - 1) / bn);
-  dim3 grid((unsigned)tiles, (unsigned)(a.batch * a.heads));
+  // Plain GEMMs run persistent workgroups, one per CU across the batch;
+  // conv GEMMs one workgroup per tile.
+  int64_t gx = tiles;
+  if (!a.conv) {
+    const int64_t z = (int64_t)a.batch * a.heads;
+    gx = std::min<int64_t>(tiles, std::max<int64_t>(1, (cu_count() + z - 1) / z));
+  }
+  dim3 grid((unsigned)gx, (unsigned)(a.batch * a.heads));
   if (dtype == MK_BF16)
     launch_gemm_t<bf16>(a, grid, st);
   else
