@@ -242,17 +242,28 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
 }
 
-// Copy rows H*16 .. H*16+15 of acc[I] (rows I*32 .. I*32+31 of this wave's
-// tile) into the wave's half slab: acc[I][j][r] with r in [8H, 8H+8) is the
-// element (row ((r/4)%2)*8 + lh*4 + r%4, column j*32 + lr), row stride LD.
-template <int I, int H, int NJ, int LD>
-__device__ __forceinline__ void stage_half(const f32x16 (&acc)[4][NJ], float* slab, int lh,
+// Epilogue staging.  In the 32 x 32 MFMA layout a lane holds, for column
+// j*32 + lr, the four consecutive rows (r/4)*8 + lh*4 + 0..3 in acc[r .. r+3]
+// (r a multiple of 4).  A wave's 32-row slab is stored as [8 row groups of 4
+// rows][kSlabU 16-byte units], unit (g, col) holding rows 4g .. 4g+3 of that
+// column, so each of those quads is one 16-byte write.  kSlabU = 64 + 1: the
+// 8 lanes reading one column unit of 8 consecutive row groups hit distinct
+// bank groups.
+constexpr int kSlabU = 65;
+
+// Copy acc[I] (rows I*32 .. I*32+31 of this wave's tile) into the slab.
+template <int I, int NJ>
+__device__ __forceinline__ void stage_slab(const f32x16 (&acc)[4][NJ], float* slab, int lh,
                                            int lr) {
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
 #pragma unroll
-    for (int r = 8 * H; r < 8 * H + 8; ++r)
-      slab[(((r >> 2) & 1) * 8 + lh * 4 + (r & 3)) * LD + j * 32 + lr] = acc[I][j][r];
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int g = 2 * r4 + lh;
+      *(f32x4*)(slab + (g * kSlabU + j * 32 + lr) * 4) =
+          f32x4{acc[I][j][4 * r4], acc[I][j][4 * r4 + 1], acc[I][j][4 * r4 + 2],
+                acc[I][j][4 * r4 + 3]};
+    }
 }
 
 // B is [N, K] (K contiguous) here; a [K, N] weight arrives pre-transposed.
@@ -265,11 +276,11 @@ __device__ __forceinline__ uint32_t conv_koff(const GemmArgs& a, int64_t k0) {
   return (uint32_t)(((r * a.cv_Wp + s) * a.cv_C + c0) * (int64_t)sizeof(T));
 }
 
-// LDS bytes of the epilogue: per wave a 16-row slab of WTN (+8) floats, then
-// the row-reduction exchange [WN][256 rows][2] floats.
+// LDS bytes of the epilogue: per wave a 32-row slab (8 row groups of kSlabU
+// 16-byte units), then the row-reduction exchange [WN][256 rows][2] floats.
 template <int WN, int BN>
 constexpr int epi_bytes() {
-  return 2 * WN * 16 * (BN / WN + 8) * 4 + WN * BM * 2 * 4;
+  return 2 * WN * 8 * kSlabU * 16 + WN * BM * 2 * 4;
 }
 
 // Variants: WN waves along N (2 rows of waves), BN columns per tile, STG
@@ -278,10 +289,9 @@ constexpr int epi_bytes() {
 //    workgroup per CU); the stages live in five 32 KB slots, three for A and
 //    two for B ([A0 | B0 | A1 | A2 | B1]), so the A loads of a stage can be
 //    spread over the stage two ahead of it.  The workgroup is persistent: it
-//    walks the tiles v = blockIdx.x, blockIdx.x + gridDim.x, ..., and issues
-//    the next tile's stage 0 and the A part of its stage 1 before the
-//    epilogue of the current one, so the epilogue's stores drain while they
-//    arrive (the epilogue's LDS region is slots A2 and B1).
+//    walks the tiles v = blockIdx.x, blockIdx.x + gridDim.x, ..., so a tile's
+//    epilogue stores drain while the next tile's first stages load.  (Loads
+//    issued before the epilogue queued ahead of its stores and slowed it.)
 //  <2, 128, 3, 1, 0, 64> (conv): four waves on a 256 x 128 tile in 72 KB of
 //    LDS, so two independent workgroups share each CU; one tile per workgroup.
 template <typename T, int WN, int BN, int STG, int CONV, int PIPE, int RB>
@@ -295,15 +305,13 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   constexpr int kStageBytes = kABytes + kBBytes;
   constexpr int WTN = BN / WN;        // wave tile columns
   constexpr int NJ = WTN / 32;        // 32-wide column tiles per wave
-  constexpr int LD = WTN + 8;         // epilogue slab row stride (floats)
-  constexpr int LPR = WTN / 8;        // lanes per slab row in the epilogue
-  constexpr int RPP = 64 / LPR;       // slab rows per pass
   constexpr bool kPersist = !CONV && PIPE != 0;
   static_assert(PIPE == 0 || (KSUB == 4 && kABytes == 32768 && kBBytes == 32768),
                 "the pipelined loop is k64 stages of a 256 x 256 tile");
-  // Pipelined slots: A0 0, B0 32K, A1 64K, A2 96K, B1 128K; the epilogue
-  // uses A2 + B1.  Ring form: stage slots back to back, epilogue at 0.
-  constexpr int kEpiOff = kPersist ? 3 * 32768 : 0;
+  // Pipelined slots: A0 0, B0 32K, A1 64K, A2 96K, B1 128K.  Ring form:
+  // stage slots back to back.  The epilogue reuses the LDS from 0.
+  constexpr int kEpiOff = 0;
+  static_assert(WTN == 64, "the epilogue maps 8 row groups x 8 column groups onto a wave");
   constexpr int kEpiEnd = kEpiOff + epi_bytes<WN, BN>();
   constexpr int kRing = PIPE ? 5 * 32768 : kStages * kStageBytes;
   constexpr int kSmem = kEpiEnd > kRing ? kEpiEnd : kRing;
@@ -366,11 +374,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   int v = blockIdx.x;
   TileCoord tc = tile_of(v, tiles_m, tiles_n);
   init_loaders(tc);
-  if (PIPE) {
-    issue_a(0);
-    issue_b(0);
-    issue_a(1);
-  } else {
+  if (!PIPE) {
 #pragma unroll
     for (int s = 0; s < kStages - 1; ++s)
       if (s < nk) {
@@ -400,12 +404,15 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   constexpr int kA0 = (LA + 1) / 2, kA1 = LA - kA0;
   static_assert(PIPE == 0 || kMfmaSub >= kReadPairs + LB + 1, "interleave needs more MFMAs");
 
-  float* slab = (float*)(smem + kEpiOff) + w * (16 * LD);
-  float* red = (float*)(smem + kEpiOff) + WAVES * 16 * LD;   // [WN column groups][256 rows][2]
+  float* slab = (float*)(smem + kEpiOff) + w * (8 * kSlabU * 4);
+  // [WN column groups][256 rows][2]
+  float* red = (float*)(smem + kEpiOff) + WAVES * 8 * kSlabU * 4;
   const int64_t cbase = a.c_off + bb * a.c_sb + hh * a.c_sh;
   T* C = (T*)a.C + cbase;
   const bool softmax = a.terminal == TERM_SOFTMAX;
-  const int q = lane % LPR;          // 8-column group within the slab row
+  // Epilogue lane roles: 8-column group q and row group rg of the slab; the
+  // 8 lanes of a row (same rg) are lanes rg, rg+8, ..., rg+56.
+  const int q = lane >> 3, rg = lane & 7;
   // 16-byte accesses to C and to residual operands need 8-aligned offsets.
   const bool vec_ok = ((a.ldc | cbase) & 7) == 0;
 
@@ -420,8 +427,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     if (PIPE) {
-      // In flight: A(0), B(0), A(1) (issued before the loop or during the
-      // previous tile's epilogue); B(1) goes now.  Stage s: sub-steps 0..3,
+      // Stages 0 and 1 go now.  Stage s: sub-steps 0..3,
       // fragments one sub-step ahead of the MFMAs that use them; A(s+2) is
       // issued over sub-steps 0 and 1 (its slot held stage s-1, released by
       // the barrier of stage s-1).  Before sub-step 3 the wave waits for its
@@ -430,8 +436,11 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       // after which stage s+1 is read and B(s+2) refills B slot s % 2.  The
       // body is branch-free: past the last stage every lane's K bound fails
       // and the loads only write zeros into slots never read again.
+      issue_a(0);
+      issue_b(0);
+      issue_a(1);
       issue_b(1);
-      wait_vm<LB>();
+      wait_vm<LA + LB>();
       __builtin_amdgcn_s_barrier();
       Frags<NJ, T> f0, f1;
       load_frags<NJ, T, RB>(a_slot(0), b_slot(0), 0, rowbase, colbase, lr, lh, f0);
@@ -516,27 +525,18 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     }
 
     // Every slot is consumed and every refill (zeros past the last stage)
-    // has landed; the next tile's A(0), B(0), A(1) go into slots A0, B0, A1,
-    // below the epilogue's region.
+    // has landed before the epilogue reuses the LDS.
     wait_vm<0>();
     __syncthreads();
     const int vn = v + (int)gridDim.x;
     const bool more = kPersist && vn < tiles;
-    TileCoord tnext = tc;
-    if (more) {
-      tnext = tile_of(vn, tiles_m, tiles_n);
-      init_loaders(tnext);
-      issue_a(0);
-      issue_b(0);
-      issue_a(1);
-    }
 
     // ---------------------------------------------------------------- epilogue
     // acc[i][j][r] is C[row, col] with
     //   row = m0 + rowbase + i*32 + (r/4)*8 + lh*4 + r%4,  col = n0 + colbase + j*32 + lr.
-    // Each wave stages 16 rows at a time in its own LDS region, then every
-    // lane applies the chain to 8 consecutive columns and writes them with one
-    // 16-byte store.
+    // Each wave stages one 32-row slab at a time in its own LDS region; lane
+    // (q, rg) then reads rows 4rg .. 4rg+3 of columns 8q .. 8q+7, applies the
+    // chain to each row's 8 values and writes them with one 16-byte store.
     const int64_t col0 = n0 + colbase + q * 8;
     const int valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
     // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0); the tile
@@ -544,19 +544,28 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     const int64_t img = CONV ? col0 / PQ : 0;
     const bool second = CONV && valid > 0 && img != (n0 < a.N ? n0 : a.N - 1) / PQ;
 
-    auto finish_half = [&](int i, int h) {
+    auto finish_slab = [&](int i) {
       __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): slab writes done (wave-private)
       __builtin_amdgcn_wave_barrier();
-      for (int pass = 0; pass < 16 / RPP; ++pass) {
-        const int rl = pass * RPP + lane / LPR;
-        const int lrow = rowbase + i * 32 + h * 16 + rl;
-        const int64_t row = m0 + lrow;
-        const float4 lo = *(const float4*)(slab + rl * LD + q * 8);
-        const float4 hi = *(const float4*)(slab + rl * LD + q * 8 + 4);
-        float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-        const bool row_ok = row < a.M;
+      f32x4 u[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] *= a.alpha;
+      for (int k = 0; k < 8; ++k) u[k] = *(const f32x4*)(slab + (rg * kSlabU + q * 8 + k) * 4);
+      // The slab is rewritten next: every lane's reads of it must be done.
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_wave_barrier();
+      // Row t of the quad is element 0 after t rotations (static indices in
+      // a loop that is not unrolled).
+#pragma unroll 1
+      for (int t = 0; t < 4; ++t) {
+        const int lrow = rowbase + i * 32 + rg * 4 + t;
+        const int64_t row = m0 + lrow;
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          v[e] = u[e][0] * a.alpha;
+          u[e] = f32x4{u[e][1], u[e][2], u[e][3], u[e][0]};
+        }
+        const bool row_ok = row < a.M;
         // Offset of (row, col0) in the output: row-major, or NCHW for a conv
         // (row = channel, col = position).
         const int64_t obase = CONV ? (img * a.M + row) * PQ + (col0 - img * PQ)
@@ -571,22 +580,22 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
           for (int e = 0; e < 8; ++e) v[e] = rnd<T>(v[e]);
         if (CONV && a.terminal == TERM_GAP) {
           // This lane's positions into the slot of their image, then over the
-          // lanes sharing the row.
+          // 8 lanes sharing the row.
           const int kind = a.pool;
-          float t = pool_id(kind);
+          float tp = pool_id(kind);
           if (kind == MK_OP_GMP) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) t = fmaxf(t, e < valid ? v[e] : -INFINITY);
+            for (int e = 0; e < 8; ++e) tp = fmaxf(tp, e < valid ? v[e] : -INFINITY);
           } else if (kind == MK_OP_LPPOOL) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) t += e < valid ? powf(v[e], a.pool_p) : 0.f;
+            for (int e = 0; e < 8; ++e) tp += e < valid ? powf(v[e], a.pool_p) : 0.f;
           } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) t += e < valid ? v[e] : 0.f;
+            for (int e = 0; e < 8; ++e) tp += e < valid ? v[e] : 0.f;
           }
-          float s0 = second ? pool_id(kind) : t, s1 = second ? t : pool_id(kind);
+          float s0 = second ? pool_id(kind) : tp, s1 = second ? tp : pool_id(kind);
 #pragma unroll
-          for (int o = LPR / 2; o > 0; o >>= 1) {
+          for (int o = 8; o < 64; o <<= 1) {
             s0 = pool_comb(kind, s0, __shfl_xor(s0, o, 64));
             s1 = pool_comb(kind, s1, __shfl_xor(s1, o, 64));
           }
@@ -624,19 +633,19 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
           }
           Moments mo{n, mean, m2};
 #pragma unroll
-          for (int o = LPR / 2; o > 0; o >>= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
+          for (int o = 8; o < 64; o <<= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
           if (q == 0) {
             red[(wn * 256 + lrow) * 2] = mo.mean;
             red[(wn * 256 + lrow) * 2 + 1] = mo.m2;
           }
         } else if (a.terminal != TERM_NONE) {
-          // reduce over the LPR lanes that share this row (this wave's columns)
+          // reduce over the 8 lanes that share this row (this wave's columns)
           float m = -INFINITY, sum = 0.f;
           if (softmax) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) m = fmaxf(m, e < valid ? v[e] : -INFINITY);
 #pragma unroll
-            for (int o = LPR / 2; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+            for (int o = 8; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
             const bool any = m != -INFINITY;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
@@ -648,31 +657,24 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
             for (int e = 0; e < 8; ++e) sum += e < valid ? v[e] : 0.f;
           }
 #pragma unroll
-          for (int o = LPR / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
+          for (int o = 8; o < 64; o <<= 1) sum += __shfl_xor(sum, o, 64);
           if (q == 0) {
             red[(wn * 256 + lrow) * 2] = m;
             red[(wn * 256 + lrow) * 2 + 1] = sum;
           }
         }
       }
-      // The slab is rewritten next: every lane's reads of it must be done.
-      __builtin_amdgcn_s_waitcnt(0xc07f);
-      __builtin_amdgcn_wave_barrier();
     };
     // A switch keeps every acc index static while the finishing code exists
     // once (the loop itself is not unrolled).
-    for (int s = 0; s < 8; ++s) {
-      switch (s) {
-        case 0: stage_half<0, 0, NJ, LD>(acc, slab, lh, lr); break;
-        case 1: stage_half<0, 1, NJ, LD>(acc, slab, lh, lr); break;
-        case 2: stage_half<1, 0, NJ, LD>(acc, slab, lh, lr); break;
-        case 3: stage_half<1, 1, NJ, LD>(acc, slab, lh, lr); break;
-        case 4: stage_half<2, 0, NJ, LD>(acc, slab, lh, lr); break;
-        case 5: stage_half<2, 1, NJ, LD>(acc, slab, lh, lr); break;
-        case 6: stage_half<3, 0, NJ, LD>(acc, slab, lh, lr); break;
-        default: stage_half<3, 1, NJ, LD>(acc, slab, lh, lr); break;
+    for (int i = 0; i < 4; ++i) {
+      switch (i) {
+        case 0: stage_slab<0, NJ>(acc, slab, lh, lr); break;
+        case 1: stage_slab<1, NJ>(acc, slab, lh, lr); break;
+        case 2: stage_slab<2, NJ>(acc, slab, lh, lr); break;
+        default: stage_slab<3, NJ>(acc, slab, lh, lr); break;
       }
-      finish_half(s >> 1, s & 1);
+      finish_slab(i);
     }
     if (a.terminal != TERM_NONE) {
       __syncthreads();
@@ -726,12 +728,13 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       }
     }
     if (!more) break;
-    // The epilogue's LDS reads are done before any wave refills slots A2 /
-    // B1, which hold its region; red is rewritten only after that loop.
+    // The epilogue's LDS accesses are done before any wave loads the next
+    // tile's stages into the same LDS.
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_s_barrier();
     v = vn;
-    tc = tnext;
+    tc = tile_of(v, tiles_m, tiles_n);
+    init_loaders(tc);
   }
 }
 
