@@ -80,8 +80,9 @@ bool impl_exists(const Plan& p, const Subkernel& sk, int impl) {
   }
 }
 
-static bool use_mfma(const Plan& p, const Subkernel& sk, int impl) {
-  if (impl != MK_IMPL_TUNED || sk.family != MK_FAM_GEMM) return false;
+// The GEMM arguments of a subkernel as far as the host decides on them
+// (operands unbound).
+static GemmArgs gemm_probe(const Subkernel& sk) {
   GemmArgs probe{};
   probe.M = sk.gemm.M;
   probe.N = sk.gemm.N;
@@ -96,7 +97,12 @@ static bool use_mfma(const Plan& p, const Subkernel& sk, int impl) {
   probe.a_off = sk.gemm.a_off; probe.a_sb = sk.gemm.a_sb; probe.a_sh = sk.gemm.a_sh;
   probe.b_off = sk.gemm.b_off; probe.b_sb = sk.gemm.b_sb; probe.b_sh = sk.gemm.b_sh;
   probe.c_off = sk.gemm.c_off; probe.c_sb = sk.gemm.c_sb; probe.c_sh = sk.gemm.c_sh;
-  return gemm_mfma_supported(p.dtype, probe);
+  return probe;
+}
+
+static bool use_mfma(const Plan& p, const Subkernel& sk, int impl) {
+  if (impl != MK_IMPL_TUNED || sk.family != MK_FAM_GEMM) return false;
+  return gemm_mfma_supported(p.dtype, gemm_probe(sk));
 }
 
 static int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
@@ -107,15 +113,15 @@ static int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
 // (mean, rstd) and normalises while loading A.
 struct GemmScratch {
   bool mfma;
-  int64_t n_tiles, ln_bytes, bt_bytes, partial_bytes;
+  int64_t tile_n, n_tiles, ln_bytes, bt_bytes, partial_bytes;
 };
 
 static GemmScratch gemm_scratch(const Plan& p, const Subkernel& sk, int impl) {
   const GemmSpec& g = sk.gemm;
   GemmScratch s{};
   s.mfma = use_mfma(p, sk, impl);
-  const int64_t tn = s.mfma ? kGemmTileN : 64;
-  s.n_tiles = (g.N + tn - 1) / tn;
+  s.tile_n = s.mfma ? gemm_mfma_tile_n(p.dtype, gemm_probe(sk)) : 64;
+  s.n_tiles = (g.N + s.tile_n - 1) / s.tile_n;
   if (g.ln) s.ln_bytes = align256(s.mfma ? g.M * g.K * elem_size(p.dtype) : 2 * g.M * 4);
   if (s.mfma && g.layout == 1) s.bt_bytes = align256(g.batch * g.heads * g.N * g.K * elem_size(p.dtype));
   if (g.terminal == TERM_ROWSUM) s.partial_bytes = align256(g.M * s.n_tiles * 4);
@@ -325,7 +331,7 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       if (g.terminal == TERM_LAYERNORM)
         return hip_check(timed([&] {
                            return launch_ln_finish(dt, a.partial, g.M, a.n_tiles, g.N,
-                                                   gs.mfma ? kGemmTileN : 64, vals[g.post_g],
+                                                   gs.tile_n, vals[g.post_g],
                                                    vals[g.post_b], g.post_eps, out, st);
                          }),
                          "layernorm finish");

@@ -845,6 +845,14 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
                        a);
 }
 
+int64_t gemm_mfma_tile_n(int dtype, const GemmArgs& a) {
+  (void)dtype;
+  if (a.conv) return kConvTileN;
+  const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + kGemmTileN - 1) / kGemmTileN) *
+                        (int64_t)a.batch * a.heads;
+  return tiles < kSmallGemmTiles ? 64 : kGemmTileN;
+}
+
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
   const int E = dtype == MK_BF16 ? 8 : 4;
   if (a.conv) {
@@ -856,6 +864,7 @@ hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
     return hipErrorInvalidValue;
   }
   if (((uintptr_t)a.A | (uintptr_t)a.B) % 16) return hipErrorInvalidValue;
+  if (!a.conv && gemm_mfma_tile_n(dtype, a) == 64) return launch_gemm_small(dtype, a, st);
   const int64_t bn = a.conv ? kConvTileN : kGemmTileN;
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + bn - 1) / bn);
   // Plain GEMMs run persistent workgroups, one per CU across the batch;

@@ -133,6 +133,13 @@ int64_t gemm_mfma_bt_bytes(int dtype, const GemmArgs& a);
 hipError_t launch_transpose_b(int dtype, const GemmArgs& a, void* dst, hipStream_t st);
 GemmArgs gemm_with_bt(const GemmArgs& a, const void* bt);
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st);
+// Column-tile width of the MFMA GEMM on these arguments: kGemmTileN, or 64
+// when the 256 x 256 grid would have fewer than kSmallGemmTiles tiles (then a
+// 64 x 64-tile kernel runs, k_gemm_small.hip); the per-tile partials of the
+// terminal finishers follow it.
+constexpr int kSmallGemmTiles = 64;
+int64_t gemm_mfma_tile_n(int dtype, const GemmArgs& a);
+hipError_t launch_gemm_small(int dtype, const GemmArgs& a, hipStream_t st);
 // Implicit-GEMM conv: pack_nhwc (x -> zero-padded NHWC), pack_krsc (w ->
 // [K][R][S][C]), the GEMM kernel in conv mode, and for a fused GAP the
 // finisher over per-tile partials.
