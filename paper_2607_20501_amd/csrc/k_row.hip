@@ -38,11 +38,11 @@ __device__ __forceinline__ void st_vec(T* p, const float* v) {
 // NV 16-byte vectors per lane cover the row (L <= 64 * NV * kEpv, L a
 // multiple of kEpv); lane l owns vectors l, l + 64, ...
 template <typename T, int NV>
-__global__ __launch_bounds__(256) void row_wave_kernel(RowArgs a) {
+__global__ __launch_bounds__(64) void row_wave_kernel(RowArgs a) {
   constexpr int E = kEpv<T>;
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= a.rows) return;   // whole wave exits together
+  const int64_t r = (int64_t)blockIdx.x;   // one wave (one row) per workgroup
+  if (r >= a.rows) return;
   const int64_t L = a.len;
   const T* x = (const T*)a.x + r * L;
   float v[NV][E];
@@ -139,7 +139,7 @@ template <typename T>
 hipError_t launch_row_wave_t(const RowArgs& a, hipStream_t st) {
   constexpr int E = kEpv<T>;
   const int64_t nv = (a.len + 64 * E - 1) / (64 * E);
-  const dim3 grid((unsigned)((a.rows + 3) / 4)), block(256);
+  const dim3 grid((unsigned)a.rows), block(64);
   switch (nv) {
     case 1: hipLaunchKernelGGL((row_wave_kernel<T, 1>), grid, block, 0, st, a); break;
     case 2: hipLaunchKernelGGL((row_wave_kernel<T, 2>), grid, block, 0, st, a); break;
@@ -267,7 +267,7 @@ bool row_wave_supported(int dtype, const RowArgs& a) {
   if (a.pre.epi.n || a.len % E || a.len > 64 * 8 * E || a.rows < 1) return false;
   if (((uintptr_t)a.x | (uintptr_t)a.y) % 16) return false;
   if (a.op == MK_OP_LAYERNORM && ((uintptr_t)a.gamma | (uintptr_t)a.beta) % 16) return false;
-  return a.rows / 4 < (1ll << 31);
+  return a.rows < (1ll << 31);   // one workgroup per row
 }
 
 hipError_t launch_row_wave(int dtype, const RowArgs& a, hipStream_t st) {
