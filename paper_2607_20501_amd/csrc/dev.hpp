@@ -138,10 +138,12 @@ __device__ __forceinline__ void st8(T* p, const float (&v)[8]) {
 // The chain applied to 8 consecutive columns col0.. of one row (flat0 is the
 // offset of column col0 in residual operands).  One uniform switch per step;
 // `vec` says that 16-byte operand accesses are aligned and in range.
+// Step `pre` (if >= 0) is a BIAS_CH whose value for this row the caller has
+// already loaded (`bpre`).
 template <typename T>
 __device__ __forceinline__ void epi_apply8(const EpiDev& e, float (&v)[8], int64_t row,
                                            int64_t col0, int64_t ch, int valid, int64_t flat0,
-                                           bool vec) {
+                                           bool vec, int pre = -1, float bpre = 0.f) {
 #pragma unroll
   for (int i = 0; i < kMaxEpi; ++i) {
     if (i >= e.n) break;
@@ -158,7 +160,7 @@ __device__ __forceinline__ void epi_apply8(const EpiDev& e, float (&v)[8], int64
         for (int k = 0; k < 8; ++k) v[k] += t[k];
         break;
       case EPI_BIAS_CH: {
-        const float bch = ld<T>((const T*)e.ptr[i], ch);
+        const float bch = i == pre ? bpre : ld<T>((const T*)e.ptr[i], ch);
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] += bch;
         break;

@@ -68,6 +68,9 @@ struct MfmaType<float> {
 };
 
 constexpr int BM = 256;
+// Epilogue signatures with straight-line code.
+constexpr int kSigGeneric = 0;
+constexpr int kSigConvBiasReluGap = 1;   // conv: channel bias, ReLU, global average pool
 constexpr int kGroupM = 8;                        // tile rows per locality group
 constexpr int kXcds = 8;
 
@@ -266,6 +269,184 @@ __device__ __forceinline__ void stage_slab(const f32x16 (&acc)[4][NJ], float* sl
     }
 }
 
+// Channel-bias values of one row tile for this lane: rows rb + (r/4)*8 +
+// lh*4 + r%4, r = 0..15, of p (zero at rows rb + mrem and beyond).
+template <typename T>
+__device__ __forceinline__ void load_row_bias(const T* p, int mrem, int lh, float (&b)[16]) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int row = (r >> 2) * 8 + lh * 4 + (r & 3);
+    b[r] = row < mrem ? ld<T>(p, row) : 0.f;
+  }
+}
+
+// The conv chain on the 16 values of one accumulator tile: rows rb + (r/4)*8
+// + lh*4 + r%4 (mrem = M - rb), at position col of image img.  One copy of
+// each step's code: the loop over the chain's steps is not unrolled.
+template <typename T>
+__device__ __forceinline__ void conv_chain16(const GemmArgs& a, float (&v)[16], int64_t rb,
+                                             int mrem, int lh, const float (&bc)[16], int pre,
+                                             bool ok, int64_t col, int64_t img, int64_t PQ) {
+#pragma unroll 1
+  for (int s = 0; s < a.epi.n; ++s) {
+    const T* p = (const T*)a.epi.ptr[s];
+    switch (a.epi.code[s]) {
+      case EPI_BIAS_CH:
+        if (s == pre) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) v[r] += bc[r];
+        } else {
+          float b[16];
+          load_row_bias<T>(p + rb, mrem, lh, b);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) v[r] += b[r];
+        }
+        break;
+      case EPI_RELU:
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = fmaxf(v[r], 0.0f);
+        break;
+      case EPI_GELU_ERF:
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = gelu_erf(v[r]);
+        break;
+      case EPI_GELU_TANH:
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = gelu_tanh(v[r]);
+        break;
+      case EPI_GELU_SIGMOID:
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] = v[r] / (1.0f + __expf(-1.702f * v[r]));
+        break;
+      case EPI_SCALE: {
+        const float sc = a.epi.s[s];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) v[r] *= sc;
+        break;
+      }
+      case EPI_ADD: {   // NCHW operand: (image, channel, position in image)
+        const T* q = p + (img * a.M + rb) * PQ + (col - img * PQ);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = (r >> 2) * 8 + lh * 4 + (r & 3);
+          if (ok && row < mrem) v[r] += ld<T>(q, (int64_t)row * PQ);
+        }
+        break;
+      }
+      default:
+        break;
+    }
+  }
+}
+
+// Global pooling of a conv tile straight from the accumulators, without
+// staging them in LDS.  Rows are channels, columns positions; lane (lr, lh)
+// holds, of row tile i, rows rowbase + i*32 + (r/4)*8 + lh*4 + r%4 (r = 0..15)
+// at columns colbase + j*32 + lr.  Per row tile: the chain on every value,
+// the pool input, its combination over the lane's NJ columns into the slot of
+// the column's image (a tile spans at most two images), and a halving
+// butterfly over the 32 lanes lr: at the step across lane bit b a lane keeps
+// the half of its values selected by that bit and adds in the partner's copy
+// of it, so after bits 4..0 lane lr holds value lr = slot*16 + r.  Results go
+// to red[wn][row][slot].  rbias: the tile's values of chain step `pre` (a
+// channel bias) in LDS, by tile row.  kBiasReluSum: the chain is exactly
+// (channel bias, ReLU) and the pool a sum (GAP), in straight-line code; the
+// general form interprets the chain and the pool kind, which costs several
+// times the time of the rest of the epilogue.
+template <typename T, int NJ, bool kBiasReluSum>
+__device__ __forceinline__ void gap_from_acc(const GemmArgs& a, const f32x16 (&acc)[4][NJ],
+                                             int64_t m0, int64_t n0, int rowbase, int colbase,
+                                             int wn, int lr, int lh, int pre,
+                                             const float* rbias, float* red) {
+  const int kind = a.pool;
+  const float pp = a.pool_p, idv = pool_id(kind);
+  const int64_t PQ = a.cv_P * a.cv_Q;
+  const int64_t img0 = n0 / PQ;
+  // columns of this lane relative to the tile, against N and the image bound
+  const int c_end = (int)min<int64_t>(a.N - n0, 1 << 30);
+  const int c_bnd = (int)min<int64_t>((img0 + 1) * PQ - n0, 1 << 30);
+#pragma unroll 1
+  for (int i = 0; i < 4; ++i) {
+    const int64_t rb = m0 + rowbase + i * 32;
+    const int mrem = (int)min<int64_t>(a.M - rb, 1 << 30);
+    float bc[16];
+    if (pre >= 0) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 q4 = *(const f32x4*)(rbias + rowbase + i * 32 + g * 8 + lh * 4);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) bc[g * 4 + t] = q4[t];
+      }
+    }
+    float x[32];   // x[slot * 16 + r]: this lane's columns, per image slot
+#pragma unroll
+    for (int k = 0; k < 32; ++k) x[k] = idv;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int cl = colbase + j * 32 + lr;
+      const bool ok = cl < c_end, s1 = cl >= c_bnd;
+      float v[16];
+      switch (i) {   // static accumulator indices
+        case 0:
+#pragma unroll
+          for (int r = 0; r < 16; ++r) v[r] = acc[0][j][r];
+          break;
+        case 1:
+#pragma unroll
+          for (int r = 0; r < 16; ++r) v[r] = acc[1][j][r];
+          break;
+        case 2:
+#pragma unroll
+          for (int r = 0; r < 16; ++r) v[r] = acc[2][j][r];
+          break;
+        default:
+#pragma unroll
+          for (int r = 0; r < 16; ++r) v[r] = acc[3][j][r];
+          break;
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) v[r] *= a.alpha;
+      if constexpr (kBiasReluSum) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float c = ok ? fmaxf(v[r] + bc[r], 0.f) : 0.f;
+          x[r] += s1 ? 0.f : c;
+          x[16 + r] += s1 ? c : 0.f;
+        }
+      } else {
+        conv_chain16<T>(a, v, rb, mrem, lh, bc, pre, ok, n0 + cl, s1 ? img0 + 1 : img0, PQ);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float c = ok ? pool_in(kind, pp, v[r]) : idv;
+          x[r] = s1 ? x[r] : pool_comb(kind, x[r], c);
+          x[16 + r] = s1 ? pool_comb(kind, x[16 + r], c) : x[16 + r];
+        }
+      }
+    }
+    // Halving butterfly over lane bits 4..0 (ds_swizzle xor within 32 lanes).
+#define MK_GAP_STEP(O, H)                                                        \
+  {                                                                              \
+    const bool up = (lr & (O)) != 0;                                             \
+    _Pragma("unroll") for (int k = 0; k < (H); ++k) {                            \
+      const float keep = up ? x[k + (H)] : x[k];                                 \
+      const float send = up ? x[k] : x[k + (H)];                                 \
+      const float got = __int_as_float(                                          \
+          __builtin_amdgcn_ds_swizzle(__float_as_int(send), ((O) << 10) | 0x1F)); \
+      x[k] = kBiasReluSum ? keep + got : pool_comb(kind, keep, got);             \
+    }                                                                            \
+  }
+    MK_GAP_STEP(16, 16)
+    MK_GAP_STEP(8, 8)
+    MK_GAP_STEP(4, 4)
+    MK_GAP_STEP(2, 2)
+    MK_GAP_STEP(1, 1)
+#undef MK_GAP_STEP
+    const int r = lr & 15, slot = lr >> 4;
+    const int lrow = rowbase + i * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+    red[(wn * 256 + lrow) * 2 + slot] = x[0];
+  }
+}
+
 // B is [N, K] (K contiguous) here; a [K, N] weight arrives pre-transposed.
 // Byte offset along K of implicit-GEMM slice k0 (k = (r*S + s)*C + c, and a
 // slice never crosses an (r, s) boundary since C is a multiple of its depth).
@@ -294,7 +475,9 @@ constexpr int epi_bytes() {
 //    issued before the epilogue queued ahead of its stores and slowed it.)
 //  <2, 128, 3, 1, 0, 64> (conv): four waves on a 256 x 128 tile in 72 KB of
 //    LDS, so two independent workgroups share each CU; one tile per workgroup.
-template <typename T, int WN, int BN, int STG, int CONV, int PIPE, int RB>
+// SIG selects an epilogue compiled for one chain (kSigGeneric: any chain,
+// interpreted step by step).
+template <typename T, int WN, int BN, int STG, int CONV, int PIPE, int RB, int SIG>
 __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kernel(GemmArgs a) {
   constexpr int BK = RB / (int)sizeof(T);   // K depth of a stage
   constexpr int KSUB = RB / 32;             // 16-byte chunk pairs (MFMA sub-steps) per stage
@@ -314,9 +497,12 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   static_assert(WTN == 64, "the epilogue maps 8 row groups x 8 column groups onto a wave");
   constexpr int kEpiEnd = kEpiOff + epi_bytes<WN, BN>();
   constexpr int kRing = PIPE ? 5 * 32768 : kStages * kStageBytes;
-  constexpr int kSmem = kEpiEnd > kRing ? kEpiEnd : kRing;
+  constexpr int kSmemMain = kEpiEnd > kRing ? kEpiEnd : kRing;
+  // Conv: the tile's channel-bias values (first BIAS_CH step) after the ring.
+  constexpr int kSmem = kSmemMain + (CONV ? BM * 4 : 0);
   static_assert(kSmem <= 163840, "LDS is 160 KB");
   __shared__ __attribute__((aligned(1024))) char smem[kSmem];
+  float* rbias = (float*)(smem + kSmemMain);
   const int tiles_m = (int)((a.M + BM - 1) / BM), tiles_n = (int)((a.N + BN - 1) / BN);
   const int tiles = tiles_m * tiles_n;
   const int64_t z = blockIdx.y, bb = z / a.heads, hh = z % a.heads;
@@ -381,6 +567,20 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         issue_a(s);
         issue_b(s);
       }
+  }
+  // Conv: the first channel-bias step of the chain (its values for the
+  // tile's rows are staged in LDS while the first stages load; conv
+  // workgroups take one tile each).
+  int pre_ch = -1;
+  if (CONV) {
+#pragma unroll
+    for (int s = 0; s < kMaxEpi; ++s)
+      if (s < a.epi.n && pre_ch < 0 && a.epi.code[s] == EPI_BIAS_CH) pre_ch = s;
+  }
+  if (CONV && pre_ch >= 0) {
+    const T* pb = (const T*)a.epi.ptr[pre_ch];
+    const int64_t m0 = (int64_t)tc.tm * BM;
+    for (int r = threadIdx.x; r < BM; r += THREADS) rbias[r] = m0 + r < a.M ? ld<T>(pb, m0 + r) : 0.f;
   }
 
   constexpr int LA = SliceLoader<WAVES, BM, T, RB>::LQ, LB = SliceLoader<WAVES, BN, T, RB>::LQ;
@@ -539,10 +739,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // chain to each row's 8 values and writes them with one 16-byte store.
     const int64_t col0 = n0 + colbase + q * 8;
     const int valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
-    // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0); the tile
-    // covers at most two, and slot 1 is the second.
+    // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0).
     const int64_t img = CONV ? col0 / PQ : 0;
-    const bool second = CONV && valid > 0 && img != (n0 < a.N ? n0 : a.N - 1) / PQ;
 
     auto finish_slab = [&](int i) {
       __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): slab writes done (wave-private)
@@ -550,6 +748,9 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       f32x4 u[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) u[k] = *(const f32x4*)(slab + (rg * kSlabU + q * 8 + k) * 4);
+      // Conv: the channel bias of this lane's 4 rows.
+      f32x4 bq = {0.f, 0.f, 0.f, 0.f};
+      if (CONV && pre_ch >= 0) bq = *(const f32x4*)(rbias + rowbase + i * 32 + rg * 4);
       // The slab is rewritten next: every lane's reads of it must be done.
       __builtin_amdgcn_s_waitcnt(0xc07f);
       __builtin_amdgcn_wave_barrier();
@@ -565,46 +766,22 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
           v[e] = u[e][0] * a.alpha;
           u[e] = f32x4{u[e][1], u[e][2], u[e][3], u[e][0]};
         }
+        const float bt = bq[0];
+        bq = f32x4{bq[1], bq[2], bq[3], bq[0]};
         const bool row_ok = row < a.M;
         // Offset of (row, col0) in the output: row-major, or NCHW for a conv
         // (row = channel, col = position).
         const int64_t obase = CONV ? (img * a.M + row) * PQ + (col0 - img * PQ)
                                    : cbase + row * a.ldc + col0;
         if (a.epi.n && row_ok && valid > 0)
-          epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok));
+          epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok),
+                        CONV ? pre_ch : -1, bt);
         // Stored values are rounded to the storage type; reductions that need
         // the whole row read them back as stored.  Below, lanes past N take
         // part through selects, not branches.
         if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX || a.terminal == TERM_LAYERNORM)
 #pragma unroll
           for (int e = 0; e < 8; ++e) v[e] = rnd<T>(v[e]);
-        if (CONV && a.terminal == TERM_GAP) {
-          // This lane's positions into the slot of their image, then over the
-          // 8 lanes sharing the row.
-          const int kind = a.pool;
-          float tp = pool_id(kind);
-          if (kind == MK_OP_GMP) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) tp = fmaxf(tp, e < valid ? v[e] : -INFINITY);
-          } else if (kind == MK_OP_LPPOOL) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) tp += e < valid ? powf(v[e], a.pool_p) : 0.f;
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) tp += e < valid ? v[e] : 0.f;
-          }
-          float s0 = second ? pool_id(kind) : tp, s1 = second ? tp : pool_id(kind);
-#pragma unroll
-          for (int o = 8; o < 64; o <<= 1) {
-            s0 = pool_comb(kind, s0, __shfl_xor(s0, o, 64));
-            s1 = pool_comb(kind, s1, __shfl_xor(s1, o, 64));
-          }
-          if (q == 0) {
-            red[(wn * 256 + lrow) * 2] = s0;
-            red[(wn * 256 + lrow) * 2 + 1] = s1;
-          }
-          continue;
-        }
         if (a.terminal != TERM_ROWSUM && row_ok) {
           // NCHW conv output is always 8-aligned (PQ % 8 == 0); a row-major
           // output needs ldc and the batch offset 8-aligned for the vector store.
@@ -665,16 +842,20 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         }
       }
     };
-    // A switch keeps every acc index static while the finishing code exists
-    // once (the loop itself is not unrolled).
-    for (int i = 0; i < 4; ++i) {
-      switch (i) {
-        case 0: stage_slab<0, NJ>(acc, slab, lh, lr); break;
-        case 1: stage_slab<1, NJ>(acc, slab, lh, lr); break;
-        case 2: stage_slab<2, NJ>(acc, slab, lh, lr); break;
-        default: stage_slab<3, NJ>(acc, slab, lh, lr); break;
+    if (SIG == kSigConvBiasReluGap || (CONV && a.terminal == TERM_GAP)) {
+      gap_from_acc<T, NJ, SIG == kSigConvBiasReluGap>(a, acc, m0, n0, rowbase, colbase, wn, lr, lh, pre_ch, rbias, red);
+    } else {
+      // A switch keeps every acc index static while the finishing code
+      // exists once (the loop itself is not unrolled).
+      for (int i = 0; i < 4; ++i) {
+        switch (i) {
+          case 0: stage_slab<0, NJ>(acc, slab, lh, lr); break;
+          case 1: stage_slab<1, NJ>(acc, slab, lh, lr); break;
+          case 2: stage_slab<2, NJ>(acc, slab, lh, lr); break;
+          default: stage_slab<3, NJ>(acc, slab, lh, lr); break;
+        }
+        finish_slab(i);
       }
-      finish_slab(i);
     }
     if (a.terminal != TERM_NONE) {
       __syncthreads();
@@ -837,12 +1018,19 @@ template <typename T>
 static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
   // (The conv variant keeps 64-byte rows and the plain three-stage ring: two
   // workgroups per CU, and C = 128 bf16 channels per filter tap.)
-  if (a.conv)
-    hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kConvTileN, 3, 1, 0, 64>), grid, dim3(256), 0, st,
-                       a);
-  else
-    hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 2, 0, 2, 128>), grid, dim3(512), 0, st,
-                       a);
+  if (a.conv) {
+    const bool brg = a.terminal == TERM_GAP && a.pool == MK_OP_GAP && a.epi.n == 2 &&
+                     a.epi.code[0] == EPI_BIAS_CH && a.epi.code[1] == EPI_RELU;
+    if (brg)
+      hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kConvTileN, 3, 1, 0, 64, kSigConvBiasReluGap>),
+                         grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kConvTileN, 3, 1, 0, 64, kSigGeneric>), grid,
+                         dim3(256), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 2, 0, 2, 128, kSigGeneric>), grid,
+                       dim3(512), 0, st, a);
+  }
 }
 
 int64_t gemm_mfma_tile_n(int dtype, const GemmArgs& a) {

@@ -6,6 +6,7 @@ import torch
 
 from helpers import describe, run_parity
 from paper_2607_20501_amd import mk, workloads
+from paper_2607_20501_amd.inputs import NORMAL, UNIFORM
 
 pytestmark = pytest.mark.gpu
 
@@ -57,3 +58,40 @@ def test_pooling_variants(shape, dec, pool, p, dtype):
     for impl in (mk.IMPL_SIMPLE,):
         rep, *_ = run_parity(module, dec, impls={i: impl for i in range(m.n)})
         assert rep["pass"], "simple: " + describe(rep)
+
+
+def _chain_module(kind, dtype):
+    """Conv modules whose fused epilogue runs longer chains: two channel
+    biases around tanh-GELU and a scale, or a residual add before ReLU."""
+    x, w = [2, 32, 20, 20], [40, 32, 3, 3]
+    rx, rw, rb = (NORMAL, 0.0, 1.0), (NORMAL, 0.0, 0.02), (UNIFORM, -0.1, 0.1)
+    conv = {"kind": "CONV2D", "in": [0, 1], "ip": [1, 1], "fp": []}
+    if kind == "gelu_scale_bias2":
+        return {"name": f"conv_chain_a_{dtype}", "dtype": dtype,
+                "inputs": [x, w, [40], [40]], "recipes": [rx, rw, rb, rb],
+                "ops": [conv, {"kind": "BIAS_CHANNEL", "in": [4, 2], "ip": [], "fp": []},
+                        {"kind": "GELU_TANH", "in": [5], "ip": [], "fp": []},
+                        {"kind": "SCALE", "in": [6], "ip": [], "fp": [0.5]},
+                        {"kind": "BIAS_CHANNEL", "in": [7, 3], "ip": [], "fp": []},
+                        {"kind": "GAP", "in": [8], "ip": [], "fp": []}]}
+    return {"name": f"conv_chain_b_{dtype}", "dtype": dtype,
+            "inputs": [x, w, [40], [2, 40, 20, 20]], "recipes": [rx, rw, rb, rx],
+            "ops": [conv, {"kind": "BIAS_CHANNEL", "in": [4, 2], "ip": [], "fp": []},
+                    {"kind": "ADD", "in": [5, 3], "ip": [], "fp": []},
+                    {"kind": "RELU", "in": [6], "ip": [], "fp": []},
+                    {"kind": "GMP", "in": [7], "ip": [], "fp": []}]}
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind", ["gelu_scale_bias2", "residual_gmp"])
+@pytest.mark.parametrize("dec", ["fused", "split"])
+def test_conv_chain_variants(kind, dec, dtype):
+    """Every chain step the conv epilogue supports, ahead of the pool (400
+    positions per image: column blocks of 32 straddle image boundaries)."""
+    print(f"conv chain {kind} {dec} {dtype}", flush=True)
+    module = _chain_module(kind, dtype)
+    rep, m, *_ = run_parity(module, dec)
+    assert m.subkernels()[0]["uses_mfma"]
+    if dec == "fused":
+        assert len(m.subkernels()) == 1
+    assert rep["pass"], describe(rep)
