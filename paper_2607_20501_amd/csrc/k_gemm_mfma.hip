@@ -51,6 +51,7 @@ namespace mk {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 namespace {
 
@@ -68,9 +69,21 @@ struct MfmaType<float> {
 };
 
 constexpr int BM = 256;
-// Epilogue signatures with straight-line code.
+// Epilogue signatures with straight-line code (kSigGeneric interprets any
+// chain step by step; the others are compiled for one chain and terminal).
 constexpr int kSigGeneric = 0;
 constexpr int kSigConvBiasReluGap = 1;   // conv: channel bias, ReLU, global average pool
+constexpr int kSigNone = 2;              // no chain, no terminal
+constexpr int kSigGeluErf = 3;           // exact GELU
+constexpr int kSigAdd = 4;               // residual add (operand laid out as C)
+constexpr int kSigBiasGeluTanhScaleSoftmax = 5;   // bias, tanh GELU, scale; softmax partials
+
+// Terminal of a signature (-1: read at run time).
+constexpr int sig_terminal(int sig) {
+  return sig == kSigBiasGeluTanhScaleSoftmax ? TERM_SOFTMAX
+         : (sig == kSigNone || sig == kSigGeluErf || sig == kSigAdd) ? TERM_NONE
+                                                                      : -1;
+}
 constexpr int kGroupM = 8;                        // tile rows per locality group
 constexpr int kXcds = 8;
 
@@ -609,7 +622,9 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   float* red = (float*)(smem + kEpiOff) + WAVES * 8 * kSlabU * 4;
   const int64_t cbase = a.c_off + bb * a.c_sb + hh * a.c_sh;
   T* C = (T*)a.C + cbase;
-  const bool softmax = a.terminal == TERM_SOFTMAX;
+  constexpr int kTerm = sig_terminal(SIG);
+  const int term = kTerm >= 0 ? kTerm : a.terminal;
+  const bool softmax = term == TERM_SOFTMAX;
   // Epilogue lane roles: 8-column group q and row group rg of the slab; the
   // 8 lanes of a row (same rg) are lanes rg, rg+8, ..., rg+56.
   const int q = lane >> 3, rg = lane & 7;
@@ -742,6 +757,119 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0).
     const int64_t img = CONV ? col0 / PQ : 0;
 
+    // Residual operand (laid out as C; range checked by signature selection).
+    const __amdgpu_buffer_rsrc_t rres =
+        make_rsrc(SIG == kSigAdd ? (const T*)a.epi.ptr[0] + cbase : (const T*)a.C,
+                  SIG == kSigAdd ? a.M * a.ldc * (int64_t)sizeof(T) : 0);
+    // Column bias of this lane's 8 columns, once per tile.
+    float bcol[8];
+    if constexpr (SIG == kSigBiasGeluTanhScaleSoftmax)
+      ld8<T>((const T*)a.epi.ptr[0] + col0, valid == 8 && vec_ok, valid, bcol);
+
+    // One row of the lane: values v of columns col0 .. col0+7 of tile row
+    // lrow; `res` is its residual piece (kSigAdd, full pieces), `bt` the conv
+    // channel bias of the row.
+    auto finish_row = [&](int lrow, float (&v)[8], const u32x4& res, float bt) {
+      const int64_t row = m0 + lrow;
+      const bool row_ok = row < a.M;
+      // Offset of (row, col0) in the output: row-major, or NCHW for a conv
+      // (row = channel, col = position).
+      const int64_t obase = CONV ? (img * a.M + row) * PQ + (col0 - img * PQ)
+                                 : cbase + row * a.ldc + col0;
+      if constexpr (SIG == kSigGeluErf) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = gelu_erf(v[e]);
+      } else if constexpr (SIG == kSigAdd) {
+        float t8[8];
+        if (valid == 8 && vec_ok) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {   // bf16 pairs, low half first
+            t8[2 * k] = __uint_as_float(res[k] << 16);
+            t8[2 * k + 1] = __uint_as_float(res[k] & 0xFFFF0000u);
+          }
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) t8[k] = 0.f;
+          if (row_ok && valid > 0) ld8<T>((const T*)a.epi.ptr[0] + obase, false, valid, t8);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] += (row_ok && e < valid) ? t8[e] : 0.f;
+      } else if constexpr (SIG == kSigBiasGeluTanhScaleSoftmax) {
+        const float sc = a.epi.s[2];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = gelu_tanh(v[e] + bcol[e]) * sc;
+      } else if constexpr (SIG == kSigGeneric || SIG == kSigConvBiasReluGap) {
+        if (a.epi.n && row_ok && valid > 0)
+          epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok),
+                        CONV ? pre_ch : -1, bt);
+      }
+      // Stored values are rounded to the storage type; reductions that need
+      // the whole row read them back as stored.  Below, lanes past N take
+      // part through selects, not branches.
+      if (term == TERM_NONE || term == TERM_SOFTMAX || term == TERM_LAYERNORM)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = rnd<T>(v[e]);
+      if (term != TERM_ROWSUM && row_ok) {
+        // NCHW conv output is always 8-aligned (PQ % 8 == 0); a row-major
+        // output needs ldc and the batch offset 8-aligned for the vector store.
+        const int64_t off = CONV ? obase : row * a.ldc + col0;
+        if (valid == 8 && (CONV || vec_ok)) {
+          st8<T>(C + off, v);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (e < valid) st<T>(C, off + e, v[e]);
+        }
+      }
+      if (term == TERM_LAYERNORM) {
+        // moments of this wave's columns of the row: mean, then the squared
+        // deviations, over the lane's valid values; lanes then merge
+        float sv = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sv += e < valid ? v[e] : 0.f;
+        const float n = (float)max(valid, 0);
+        const float mean = valid > 0 ? sv / n : 0.f;
+        float m2 = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float d = v[e] - mean;
+          m2 += e < valid ? d * d : 0.f;
+        }
+        Moments mo{n, mean, m2};
+#pragma unroll
+        for (int o = 8; o < 64; o <<= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
+        if (q == 0) {
+          red[(wn * 256 + lrow) * 2] = mo.mean;
+          red[(wn * 256 + lrow) * 2 + 1] = mo.m2;
+        }
+      } else if (term != TERM_NONE) {
+        // reduce over the 8 lanes that share this row (this wave's columns)
+        float m = -INFINITY, sum = 0.f;
+        if (softmax) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) m = fmaxf(m, e < valid ? v[e] : -INFINITY);
+#pragma unroll
+          for (int o = 8; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+          const bool any = m != -INFINITY;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float x = __expf(v[e] - m);
+            sum += (e < valid && any) ? x : 0.f;
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) sum += e < valid ? v[e] : 0.f;
+        }
+#pragma unroll
+        for (int o = 8; o < 64; o <<= 1) sum += __shfl_xor(sum, o, 64);
+        if (q == 0) {
+          red[(wn * 256 + lrow) * 2] = m;
+          red[(wn * 256 + lrow) * 2 + 1] = sum;
+        }
+      }
+    };
+
+    // Generic form: one slab at a time, rows in a loop that is not unrolled.
     auto finish_slab = [&](int i) {
       __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): slab writes done (wave-private)
       __builtin_amdgcn_wave_barrier();
@@ -758,8 +886,6 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       // a loop that is not unrolled).
 #pragma unroll 1
       for (int t = 0; t < 4; ++t) {
-        const int lrow = rowbase + i * 32 + rg * 4 + t;
-        const int64_t row = m0 + lrow;
         float v[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -768,82 +894,58 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         }
         const float bt = bq[0];
         bq = f32x4{bq[1], bq[2], bq[3], bq[0]};
-        const bool row_ok = row < a.M;
-        // Offset of (row, col0) in the output: row-major, or NCHW for a conv
-        // (row = channel, col = position).
-        const int64_t obase = CONV ? (img * a.M + row) * PQ + (col0 - img * PQ)
-                                   : cbase + row * a.ldc + col0;
-        if (a.epi.n && row_ok && valid > 0)
-          epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok),
-                        CONV ? pre_ch : -1, bt);
-        // Stored values are rounded to the storage type; reductions that need
-        // the whole row read them back as stored.  Below, lanes past N take
-        // part through selects, not branches.
-        if (a.terminal == TERM_NONE || a.terminal == TERM_SOFTMAX || a.terminal == TERM_LAYERNORM)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = rnd<T>(v[e]);
-        if (a.terminal != TERM_ROWSUM && row_ok) {
-          // NCHW conv output is always 8-aligned (PQ % 8 == 0); a row-major
-          // output needs ldc and the batch offset 8-aligned for the vector store.
-          const int64_t off = CONV ? obase : row * a.ldc + col0;
-          if (valid == 8 && (CONV || vec_ok)) {
-            st8<T>(C + off, v);
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (e < valid) st<T>(C, off + e, v[e]);
-          }
-        }
-        if (a.terminal == TERM_LAYERNORM) {
-          // moments of this wave's columns of the row: mean, then the squared
-          // deviations, over the lane's valid values; lanes then merge
-          float sv = 0.f;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) sv += e < valid ? v[e] : 0.f;
-          const float n = (float)max(valid, 0);
-          const float mean = valid > 0 ? sv / n : 0.f;
-          float m2 = 0.f;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float d = v[e] - mean;
-            m2 += e < valid ? d * d : 0.f;
-          }
-          Moments mo{n, mean, m2};
-#pragma unroll
-          for (int o = 8; o < 64; o <<= 1) mo = mom_comb(mo, mom_shfl_xor(mo, o));
-          if (q == 0) {
-            red[(wn * 256 + lrow) * 2] = mo.mean;
-            red[(wn * 256 + lrow) * 2 + 1] = mo.m2;
-          }
-        } else if (a.terminal != TERM_NONE) {
-          // reduce over the 8 lanes that share this row (this wave's columns)
-          float m = -INFINITY, sum = 0.f;
-          if (softmax) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) m = fmaxf(m, e < valid ? v[e] : -INFINITY);
-#pragma unroll
-            for (int o = 8; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-            const bool any = m != -INFINITY;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const float x = __expf(v[e] - m);
-              sum += (e < valid && any) ? x : 0.f;
-            }
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) sum += e < valid ? v[e] : 0.f;
-          }
-#pragma unroll
-          for (int o = 8; o < 64; o <<= 1) sum += __shfl_xor(sum, o, 64);
-          if (q == 0) {
-            red[(wn * 256 + lrow) * 2] = m;
-            red[(wn * 256 + lrow) * 2 + 1] = sum;
-          }
-        }
+        finish_row(rowbase + i * 32 + rg * 4 + t, v, u32x4{0, 0, 0, 0}, bt);
       }
     };
-    if (SIG == kSigConvBiasReluGap || (CONV && a.terminal == TERM_GAP)) {
+
+    // Residual pieces of this lane's 4 rows of slab i, as buffer loads (a
+    // lane without a full piece reads zeros, with no branch to wait at).
+    auto load_res = [&](int i, u32x4 (&dst)[4]) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int64_t row = m0 + rowbase + i * 32 + rg * 4 + t;
+        const bool full = row < a.M && valid == 8 && vec_ok;
+        const uint32_t off = full ? (uint32_t)((row * a.ldc + col0) * (int64_t)sizeof(T)) : kOob;
+        dst[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rres, (int)off, 0, 0));
+      }
+    };
+    // Compiled chains: slabs and rows unrolled (static indices).  The
+    // residual pieces of slab I+1 are requested before slab I's stores: loads
+    // and stores share one in-order counter, so a load issued after a store
+    // could only be waited for together with that store.
+    auto finish_slab_sig = [&](auto I_, u32x4 (&cur)[4], u32x4 (&nxt)[4]) {
+      constexpr int I = decltype(I_)::value;
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_wave_barrier();
+      f32x4 u[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) u[k] = *(const f32x4*)(slab + (rg * kSlabU + q * 8 + k) * 4);
+      if constexpr (SIG == kSigAdd && I < 3) load_res(I + 1, nxt);
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = u[e][t] * a.alpha;
+        finish_row(rowbase + I * 32 + rg * 4 + t, v, cur[t], 0.f);
+      }
+    };
+    if (SIG == kSigConvBiasReluGap || (CONV && term == TERM_GAP)) {
       gap_from_acc<T, NJ, SIG == kSigConvBiasReluGap>(a, acc, m0, n0, rowbase, colbase, wn, lr, lh, pre_ch, rbias, red);
+    } else if constexpr (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd) {
+      // (The softmax-partial chain keeps the rolled loop: unrolled, its
+      // live values spill.)
+      u32x4 ra[4], rb[4];
+      if constexpr (SIG == kSigAdd) load_res(0, ra);
+      stage_slab<0, NJ>(acc, slab, lh, lr);
+      finish_slab_sig(std::integral_constant<int, 0>{}, ra, rb);
+      stage_slab<1, NJ>(acc, slab, lh, lr);
+      finish_slab_sig(std::integral_constant<int, 1>{}, rb, ra);
+      stage_slab<2, NJ>(acc, slab, lh, lr);
+      finish_slab_sig(std::integral_constant<int, 2>{}, ra, rb);
+      stage_slab<3, NJ>(acc, slab, lh, lr);
+      finish_slab_sig(std::integral_constant<int, 3>{}, rb, ra);
     } else {
       // A switch keeps every acc index static while the finishing code
       // exists once (the loop itself is not unrolled).
@@ -857,7 +959,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         finish_slab(i);
       }
     }
-    if (a.terminal != TERM_NONE) {
+    if (term != TERM_NONE) {
       __syncthreads();
       for (int lrow = threadIdx.x; lrow < BM; lrow += THREADS) {
         const int64_t row = m0 + lrow;
@@ -874,8 +976,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
           continue;
         }
         float* part = a.partial + (row * a.n_tiles + tc.tn) *
-                                      (softmax || a.terminal == TERM_LAYERNORM ? 2 : 1);
-        if (a.terminal == TERM_LAYERNORM) {
+                                      (softmax || term == TERM_LAYERNORM ? 2 : 1);
+        if (term == TERM_LAYERNORM) {
           // combine the WN waves' column ranges (their counts follow from N)
           Moments mo{0.f, 0.f, 0.f};
 #pragma unroll
@@ -1014,6 +1116,24 @@ static int cu_count() {
   return cache[dev];
 }
 
+// The compiled epilogue for a plain GEMM's chain and terminal (kSigGeneric if
+// none matches).
+static int gemm_signature(const GemmArgs& a) {
+  const EpiDev& e = a.epi;
+  if (a.terminal == TERM_NONE) {
+    if (e.n == 0) return kSigNone;
+    if (e.n == 1 && e.code[0] == EPI_GELU_ERF) return kSigGeluErf;
+    // (the residual is read through a buffer resource: 32-bit byte range)
+    if (e.n == 1 && e.code[0] == EPI_ADD && a.batch * a.heads == 1 &&
+        a.M * a.ldc * 2 < ((int64_t)1 << 31))
+      return kSigAdd;
+  } else if (a.terminal == TERM_SOFTMAX && e.n == 3 && e.code[0] == EPI_BIAS_COL &&
+             e.code[1] == EPI_GELU_TANH && e.code[2] == EPI_SCALE) {
+    return kSigBiasGeluTanhScaleSoftmax;
+  }
+  return kSigGeneric;
+}
+
 template <typename T>
 static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
   // (The conv variant keeps 64-byte rows and the plain three-stage ring: two
@@ -1027,9 +1147,24 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
     else
       hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kConvTileN, 3, 1, 0, 64, kSigGeneric>), grid,
                          dim3(256), 0, st, a);
-  } else {
+  } else if constexpr (sizeof(T) != 2) {
     hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 2, 0, 2, 128, kSigGeneric>), grid,
                        dim3(512), 0, st, a);
+  } else {
+    switch (gemm_signature(a)) {
+#define MK_GEMM_SIG(SIG)                                                                      \
+  case SIG:                                                                                   \
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 2, 0, 2, 128, SIG>), grid, dim3(512), \
+                       0, st, a);                                                             \
+    break;
+      MK_GEMM_SIG(kSigNone)
+      MK_GEMM_SIG(kSigGeluErf)
+      MK_GEMM_SIG(kSigAdd)
+      MK_GEMM_SIG(kSigBiasGeluTanhScaleSoftmax)
+      default:
+        MK_GEMM_SIG(kSigGeneric)
+#undef MK_GEMM_SIG
+    }
   }
 }
 

@@ -171,3 +171,32 @@ def test_post_ln_ffn_block(shape, dec, dtype):
         assert m.subkernels()[1]["uses_mfma"] and m.subkernels()[1]["n_launches"] == 2
     rep, *_ = run_parity(module, dec, impls={i: mk.IMPL_SIMPLE for i in range(m.n)})
     assert rep["pass"], "simple: " + describe(rep)
+
+
+# At least 64 tiles of 256 x 256 (smaller problems take the 64 x 64 kernel),
+# ragged in M and N; the chains compiled into their own epilogues (none, exact
+# GELU, residual add, bias + tanh GELU + scale + softmax partials) and the
+# interpreted chain.  N = 2053 makes the output rows unaligned for 16-byte
+# stores (element-wise tail path).
+BIG_CHAINS = [(), ("GELU_ERF",), ("ADD",), ("BIAS", "GELU_TANH", "SCALE", "SOFTMAX"),
+              ("BIAS", "GELU_ERF", "SCALE", "ADD"), ("ROWSUM",)]
+
+
+@pytest.mark.parametrize("epi", BIG_CHAINS, ids=lambda e: "+".join(e) or "none")
+@pytest.mark.parametrize("M,N,layout", [(2100, 2056, 0), (2100, 2056, 1), (2071, 2053, 0)])
+def test_gemm_big_tiles(M, N, layout, epi):
+    print(f"gemm big {M}x{N} layout {layout} {epi}", flush=True)
+    module = gemm_module(M, N, 136, layout, epi=epi)
+    rep, m, out, *_ = run_parity(module, [0] * (1 + len(epi)))
+    assert m.subkernels()[0]["uses_mfma"]
+    assert rep["pass"], describe(rep)
+    if "SOFTMAX" in epi:
+        np.testing.assert_allclose(mk.to_float64(out).sum(-1), 1.0, atol=1e-2)
+
+
+@pytest.mark.parametrize("epi", [(), ("BIAS", "GELU_TANH", "SCALE", "SOFTMAX")],
+                         ids=lambda e: "+".join(e) or "none")
+def test_gemm_big_tiles_f32(epi):
+    module = gemm_module(2100, 2056, 72, 0, dtype="f32", epi=epi)
+    rep, m, *_ = run_parity(module, [0] * (1 + len(epi)))
+    assert rep["pass"], describe(rep)
