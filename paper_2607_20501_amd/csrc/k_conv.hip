@@ -129,7 +129,9 @@ bool conv_mfma_supported(int dtype, const ConvArgs& a) {
   // (r, s) boundary; 8 consecutive positions stay in one image.
   const int64_t bk = dtype == MK_BF16 ? 32 : 16;
   if (a.C % bk || (a.P * a.Q) % 8) return false;
-  if (a.gap && a.P * a.Q < kConvTileN) return false;   // a tile spans at most two images
+  // a tile spans at most two images
+  if (a.gap && a.P * a.Q < conv_gemm_tile_n(dtype, a.C, a.P * a.Q, a.epi, a.gap, a.pool))
+    return false;
   const int64_t xp = a.N * (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C * esize(dtype);
   return xp < ((int64_t)1 << 31) && a.K * a.R * a.S * a.C * esize(dtype) < ((int64_t)1 << 31);
 }
@@ -139,7 +141,8 @@ ConvScratch conv_mfma_scratch(int dtype, const ConvArgs& a) {
   auto al = [](int64_t b) { return (b + 255) / 256 * 256; };
   s.xp_bytes = al(a.N * (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C * esize(dtype));
   s.wp_bytes = al(a.K * a.R * a.S * a.C * esize(dtype));
-  const int64_t tiles = (a.N * a.P * a.Q + kConvTileN - 1) / kConvTileN;
+  const int64_t tn = conv_gemm_tile_n(dtype, a.C, a.P * a.Q, a.epi, a.gap, a.pool);
+  const int64_t tiles = (a.N * a.P * a.Q + tn - 1) / tn;
   s.partial_bytes = a.gap ? al(tiles * 2 * a.K * 4) : 0;
   return s;
 }
@@ -196,7 +199,8 @@ GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float
   g.pool = a.pool;
   g.pool_p = a.pool_p;
   g.partial = partial;
-  g.n_tiles = (g.N + kConvTileN - 1) / kConvTileN;
+  // (n_tiles is not read in conv mode: partials are indexed by tile.)
+  g.n_tiles = 0;
   g.conv = 1;
   g.cv_C = a.C;
   g.cv_Hp = a.H + 2 * a.pad;
@@ -210,13 +214,14 @@ GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float
 
 hipError_t launch_gap_finish(int dtype, const ConvArgs& a, const float* partial, hipStream_t st) {
   const int64_t total = a.N * a.K;
+  const int64_t tn = conv_gemm_tile_n(dtype, a.C, a.P * a.Q, a.epi, a.gap, a.pool);
   const dim3 grid((unsigned)((total + 255) / 256));
   if (dtype == MK_BF16)
     hipLaunchKernelGGL(gap_finish_kernel<bf16>, grid, dim3(256), 0, st, partial, a.N, a.K,
-                       a.P * a.Q, (int64_t)kConvTileN, (int)a.pool, a.pool_p, (bf16*)a.y);
+                       a.P * a.Q, tn, (int)a.pool, a.pool_p, (bf16*)a.y);
   else
     hipLaunchKernelGGL(gap_finish_kernel<float>, grid, dim3(256), 0, st, partial, a.N, a.K,
-                       a.P * a.Q, (int64_t)kConvTileN, (int)a.pool, a.pool_p, (float*)a.y);
+                       a.P * a.Q, tn, (int)a.pool, a.pool_p, (float*)a.y);
   return hipGetLastError();
 }
 

@@ -501,21 +501,27 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   constexpr int kStageBytes = kABytes + kBBytes;
   constexpr int WTN = BN / WN;        // wave tile columns
   constexpr int NJ = WTN / 32;        // 32-wide column tiles per wave
-  constexpr bool kPersist = !CONV && PIPE != 0;
+  constexpr bool kPersist = PIPE != 0;
   static_assert(PIPE == 0 || (KSUB == 4 && kABytes == 32768 && kBBytes == 32768),
                 "the pipelined loop is k64 stages of a 256 x 256 tile");
-  // Pipelined slots: A0 0, B0 32K, A1 64K, A2 96K, B1 128K.  Ring form:
-  // stage slots back to back.  The epilogue reuses the LDS from 0.
-  constexpr int kEpiOff = 0;
+  // Pipelined slots: A0 0, B0 32K, A1 64K, A2 96K, B1 128K; the epilogue
+  // reuses the top of the LDS (clear of A0 and B0, which take the next tile's
+  // stage 0 meanwhile).  Ring form: stage slots back to back, the epilogue
+  // from 0.
   static_assert(WTN == 64, "the epilogue maps 8 row groups x 8 column groups onto a wave");
-  constexpr int kEpiEnd = kEpiOff + epi_bytes<WN, BN>();
   constexpr int kRing = PIPE ? 5 * 32768 : kStages * kStageBytes;
+  constexpr int kEpiOff = PIPE ? ((kRing - epi_bytes<WN, BN>()) & ~1023) : 0;
+  static_assert(PIPE == 0 || kEpiOff >= 65536, "the epilogue must leave A0 and B0 free");
+  constexpr int kEpiEnd = kEpiOff + epi_bytes<WN, BN>();
   constexpr int kSmemMain = kEpiEnd > kRing ? kEpiEnd : kRing;
   // Conv: the tile's channel-bias values (first BIAS_CH step) after the ring.
-  constexpr int kSmem = kSmemMain + (CONV ? BM * 4 : 0);
+  // Conv: the tile's channel-bias values (first BIAS_CH step): after the
+  // ring, or (pipelined form, whose slots fill the LDS) at the start of the
+  // epilogue region, unused by the pooling epilogue.
+  constexpr int kSmem = kSmemMain + (CONV && !PIPE ? BM * 4 : 0);
   static_assert(kSmem <= 163840, "LDS is 160 KB");
   __shared__ __attribute__((aligned(1024))) char smem[kSmem];
-  float* rbias = (float*)(smem + kSmemMain);
+  float* rbias = (float*)(smem + (PIPE ? kEpiOff : kSmemMain));
   const int tiles_m = (int)((a.M + BM - 1) / BM), tiles_n = (int)((a.N + BN - 1) / BN);
   const int tiles = tiles_m * tiles_n;
   const int64_t z = blockIdx.y, bb = z / a.heads, hh = z % a.heads;
@@ -590,7 +596,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     for (int s = 0; s < kMaxEpi; ++s)
       if (s < a.epi.n && pre_ch < 0 && a.epi.code[s] == EPI_BIAS_CH) pre_ch = s;
   }
-  if (CONV && pre_ch >= 0) {
+  if (CONV && !PIPE && pre_ch >= 0) {
     const T* pb = (const T*)a.epi.ptr[pre_ch];
     const int64_t m0 = (int64_t)tc.tm * BM;
     for (int r = threadIdx.x; r < BM; r += THREADS) rbias[r] = m0 + r < a.M ? ld<T>(pb, m0 + r) : 0.f;
@@ -617,20 +623,29 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   constexpr int kA0 = (LA + 1) / 2, kA1 = LA - kA0;
   static_assert(PIPE == 0 || kMfmaSub >= kReadPairs + LB + 1, "interleave needs more MFMAs");
 
-  float* slab = (float*)(smem + kEpiOff) + w * (8 * kSlabU * 4);
-  // [WN column groups][256 rows][2]
+  // Row-reduction exchange [WN column groups][256 rows][2], after the slabs
+  // (each wave's 32-row slab: 8 row groups of kSlabU 16-byte units).
   float* red = (float*)(smem + kEpiOff) + WAVES * 8 * kSlabU * 4;
   const int64_t cbase = a.c_off + bb * a.c_sb + hh * a.c_sh;
   T* C = (T*)a.C + cbase;
   constexpr int kTerm = sig_terminal(SIG);
   const int term = kTerm >= 0 ? kTerm : a.terminal;
   const bool softmax = term == TERM_SOFTMAX;
-  // Epilogue lane roles: 8-column group q and row group rg of the slab; the
-  // 8 lanes of a row (same rg) are lanes rg, rg+8, ..., rg+56.
-  const int q = lane >> 3, rg = lane & 7;
   // 16-byte accesses to C and to residual operands need 8-aligned offsets.
   const bool vec_ok = ((a.ldc | cbase) & 7) == 0;
 
+  // Pipelined conv: this thread's channel-bias value of the tile (rows
+  // threadIdx.x < BM), loaded with the tile's first stages and written to LDS
+  // once the main loop has released it.
+  auto load_bias_reg = [&](const TileCoord& t) -> float {
+    if (!(CONV && PIPE) || pre_ch < 0 || (int)threadIdx.x >= BM) return 0.f;
+    const int64_t r = (int64_t)t.tm * BM + threadIdx.x;
+    return r < a.M ? ld<T>((const T*)a.epi.ptr[pre_ch], r) : 0.f;
+  };
+  float bias_reg = load_bias_reg(tc);
+  bool staged0 = false;   // this tile's stage 0 was issued during the last epilogue
+  constexpr int kEpiVmem =
+      (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd) ? 16 : 0;
   for (;;) {
     const int64_t m0 = (int64_t)tc.tm * BM, n0 = (int64_t)tc.tn * BN;
     f32x16 acc[4][NJ];
@@ -651,11 +666,20 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       // after which stage s+1 is read and B(s+2) refills B slot s % 2.  The
       // body is branch-free: past the last stage every lane's K bound fails
       // and the loads only write zeros into slots never read again.
-      issue_a(0);
-      issue_b(0);
+      // After a prefetched stage 0 the last epilogue's memory operations sit
+      // between the two stages: kEpiVmem of them at least (each of its 16
+      // rows issues a store in the buffer-store forms), so that many may stay
+      // outstanding with stage 1 (otherwise the wait covers them too).
+      if (!staged0) {
+        issue_a(0);
+        issue_b(0);
+      }
       issue_a(1);
       issue_b(1);
-      wait_vm<LA + LB>();
+      if (staged0)
+        wait_vm<LA + LB + kEpiVmem>();
+      else
+        wait_vm<LA + LB>();
       __builtin_amdgcn_s_barrier();
       Frags<NJ, T> f0, f1;
       load_frags<NJ, T, RB>(a_slot(0), b_slot(0), 0, rowbase, colbase, lr, lh, f0);
@@ -743,8 +767,39 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // has landed before the epilogue reuses the LDS.
     wait_vm<0>();
     __syncthreads();
+    if (CONV && PIPE && pre_ch >= 0) {
+      if ((int)threadIdx.x < BM) rbias[threadIdx.x] = bias_reg;
+      __syncthreads();
+    }
     const int vn = v + (int)gridDim.x;
     const bool more = kPersist && vn < tiles;
+    // The next tile's stage 0 loads while this epilogue runs (its LDS is
+    // clear of slots A0 and B0; every read of the last stages is done).
+    TileCoord tc_next = tc;
+    if (PIPE && more) {
+      tc_next = tile_of(vn, tiles_m, tiles_n);
+      init_loaders(tc_next);
+      issue_a(0);
+      issue_b(0);
+      bias_reg = load_bias_reg(tc_next);
+    }
+    staged0 = PIPE && more;
+    // Lane-derived values of the epilogue, recomputed here from an opaque
+    // copy of the thread index: otherwise they are hoisted out of the tile
+    // loop, live across the main loop and spill (each reload then waits for
+    // every store before it).  lr, lh, rowbase, colbase and wn shadow the
+    // kernel-wide ones.
+    int tid_e = (int)threadIdx.x;
+    asm volatile("" : "+v"(tid_e));
+    const int lane_e = tid_e & 63, w_e = tid_e >> 6;
+    const int wn_e = w_e % WN;
+    const int lr = lane_e & 31, lh = lane_e >> 5;
+    const int rowbase = (w_e / WN) * 128, colbase = wn_e * WTN;
+    // Epilogue lane roles: 8-column group q and row group rg of the slab;
+    // the 8 lanes of a row (same rg) are lanes rg, rg+8, ..., rg+56.
+    const int q = lane_e >> 3, rg = lane_e & 7;
+    const int wn = wn_e;
+    float* slab = (float*)(smem + kEpiOff) + w_e * (8 * kSlabU * 4);
 
     // ---------------------------------------------------------------- epilogue
     // acc[i][j][r] is C[row, col] with
@@ -757,6 +812,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0).
     const int64_t img = CONV ? col0 / PQ : 0;
 
+    // Compiled TERM_NONE chains store through a buffer resource over C.
+    constexpr bool kBufStore = SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd;
+    const __amdgpu_buffer_rsrc_t rcst =
+        make_rsrc(C, kBufStore ? a.M * a.ldc * (int64_t)sizeof(T) : 0);
     // Residual operand (laid out as C; range checked by signature selection).
     const __amdgpu_buffer_rsrc_t rres =
         make_rsrc(SIG == kSigAdd ? (const T*)a.epi.ptr[0] + cbase : (const T*)a.C,
@@ -809,7 +868,24 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       if (term == TERM_NONE || term == TERM_SOFTMAX || term == TERM_LAYERNORM)
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = rnd<T>(v[e]);
-      if (term != TERM_ROWSUM && row_ok) {
+      if constexpr (kBufStore) {
+        // 32-bit offsets into C (range checked at selection); rows past M and
+        // columns past N get offsets beyond the range and are dropped.
+        const int r32 = (int)m0 + lrow;
+        const uint32_t roff = row_ok ? (uint32_t)((r32 * (int)a.ldc + (int)col0) * 2) : kOob;
+        if (valid == 8 && vec_ok) {
+          u32x4 o;
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            o[k] = (uint32_t)f2bf(v[2 * k]) | ((uint32_t)f2bf(v[2 * k + 1]) << 16);
+          __builtin_amdgcn_raw_buffer_store_b128(o, rcst, (int)roff, 0, 0);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            __builtin_amdgcn_raw_buffer_store_b16(f2bf(v[e]), rcst,
+                                                  (int)(e < valid ? roff + 2 * e : kOob), 0, 0);
+        }
+      } else if (term != TERM_ROWSUM && row_ok) {
         // NCHW conv output is always 8-aligned (PQ % 8 == 0); a row-major
         // output needs ldc and the batch offset 8-aligned for the vector store.
         const int64_t off = CONV ? obase : row * a.ldc + col0;
@@ -1012,12 +1088,11 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     }
     if (!more) break;
     // The epilogue's LDS accesses are done before any wave loads the next
-    // tile's stages into the same LDS.
+    // tile's stage 1 (slot A1 overlaps the epilogue's LDS).
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_s_barrier();
     v = vn;
-    tc = tile_of(v, tiles_m, tiles_n);
-    init_loaders(tc);
+    tc = tc_next;
   }
 }
 
@@ -1120,13 +1195,13 @@ static int cu_count() {
 // none matches).
 static int gemm_signature(const GemmArgs& a) {
   const EpiDev& e = a.epi;
-  if (a.terminal == TERM_NONE) {
+  // (C and a residual are addressed through buffer resources: one batch,
+  // 32-bit byte range)
+  const bool buf = a.batch * a.heads == 1 && a.M * a.ldc * 2 < ((int64_t)1 << 31);
+  if (a.terminal == TERM_NONE && buf) {
     if (e.n == 0) return kSigNone;
     if (e.n == 1 && e.code[0] == EPI_GELU_ERF) return kSigGeluErf;
-    // (the residual is read through a buffer resource: 32-bit byte range)
-    if (e.n == 1 && e.code[0] == EPI_ADD && a.batch * a.heads == 1 &&
-        a.M * a.ldc * 2 < ((int64_t)1 << 31))
-      return kSigAdd;
+    if (e.n == 1 && e.code[0] == EPI_ADD) return kSigAdd;
   } else if (a.terminal == TERM_SOFTMAX && e.n == 3 && e.code[0] == EPI_BIAS_COL &&
              e.code[1] == EPI_GELU_TANH && e.code[2] == EPI_SCALE) {
     return kSigBiasGeluTanhScaleSoftmax;
@@ -1134,14 +1209,41 @@ static int gemm_signature(const GemmArgs& a) {
   return kSigGeneric;
 }
 
+// The conv chain (channel bias, ReLU) ending in an average pool.
+static bool conv_bias_relu_gap(const EpiDev& epi, bool gap, int pool) {
+  return gap && pool == MK_OP_GAP && epi.n == 2 && epi.code[0] == EPI_BIAS_CH &&
+         epi.code[1] == EPI_RELU;
+}
+
+bool conv_bias_relu_gap_wide(int dtype, int64_t C, int64_t PQ, const EpiDev& epi, bool gap,
+                             int pool) {
+  // bf16 only (fp32 MFMAs run four times longer per tile, and the ring form
+  // with two workgroups per CU measured faster there); 128-byte rows of
+  // channels; a 256-position tile spans at most two images (PQ >= 256).
+  return dtype == MK_BF16 && conv_bias_relu_gap(epi, gap, pool) && C % 64 == 0 && PQ >= 256;
+}
+
+int64_t conv_gemm_tile_n(int dtype, int64_t C, int64_t PQ, const EpiDev& epi, bool gap,
+                         int pool) {
+  return conv_bias_relu_gap_wide(dtype, C, PQ, epi, gap, pool) ? 256 : kConvTileN;
+}
+
+static bool conv_wide(int dtype, const GemmArgs& a) {
+  return a.conv && conv_bias_relu_gap_wide(dtype, a.cv_C, a.cv_P * a.cv_Q, a.epi,
+                                           a.terminal == TERM_GAP, a.pool);
+}
+
 template <typename T>
 static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
-  // (The conv variant keeps 64-byte rows and the plain three-stage ring: two
-  // workgroups per CU, and C = 128 bf16 channels per filter tap.)
+  // Conv GEMMs: the bf16 (channel bias, ReLU, average pool) chain on the
+  // persistent 256 x 256 kernel; the rest keep 64-byte rows and the
+  // three-stage ring (two workgroups per CU; a slice of 32 bf16 channels stays
+  // in one tap), with that chain compiled in where it applies.
   if (a.conv) {
-    const bool brg = a.terminal == TERM_GAP && a.pool == MK_OP_GAP && a.epi.n == 2 &&
-                     a.epi.code[0] == EPI_BIAS_CH && a.epi.code[1] == EPI_RELU;
-    if (brg)
+    if (conv_wide(sizeof(T) == 2 ? MK_BF16 : MK_F32, a))
+      hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, 256, 2, 1, 2, 128, kSigConvBiasReluGap>), grid,
+                         dim3(512), 0, st, a);
+    else if (conv_bias_relu_gap(a.epi, a.terminal == TERM_GAP, a.pool))
       hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kConvTileN, 3, 1, 0, 64, kSigConvBiasReluGap>),
                          grid, dim3(256), 0, st, a);
     else
@@ -1169,8 +1271,7 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
 }
 
 int64_t gemm_mfma_tile_n(int dtype, const GemmArgs& a) {
-  (void)dtype;
-  if (a.conv) return kConvTileN;
+  if (a.conv) return conv_wide(dtype, a) ? 256 : kConvTileN;
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + kGemmTileN - 1) / kGemmTileN) *
                         (int64_t)a.batch * a.heads;
   return tiles < kSmallGemmTiles ? 64 : kGemmTileN;
@@ -1179,7 +1280,7 @@ int64_t gemm_mfma_tile_n(int dtype, const GemmArgs& a) {
 hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
   const int E = dtype == MK_BF16 ? 8 : 4;
   if (a.conv) {
-    const int BKe = dtype == MK_BF16 ? 32 : 16;   // slice depth
+    const int BKe = (dtype == MK_BF16 ? 32 : 16) * (conv_wide(dtype, a) ? 2 : 1);   // slice depth
     if ((dtype != MK_BF16 && dtype != MK_F32) || a.cv_C % BKe || (a.cv_P * a.cv_Q) % 8 ||
         a.lda % E || a.K % BKe)
       return hipErrorInvalidValue;
@@ -1188,12 +1289,12 @@ hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
   }
   if (((uintptr_t)a.A | (uintptr_t)a.B) % 16) return hipErrorInvalidValue;
   if (!a.conv && gemm_mfma_tile_n(dtype, a) == 64) return launch_gemm_small(dtype, a, st);
-  const int64_t bn = a.conv ? kConvTileN : kGemmTileN;
+  const int64_t bn = gemm_mfma_tile_n(dtype, a);
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + bn - 1) / bn);
-  // Plain GEMMs run persistent workgroups, one per CU across the batch;
-  // conv GEMMs one workgroup per tile.
+  // The 256 x 256 kernels run persistent workgroups, one per CU across the
+  // batch; the ring conv kernel one workgroup per tile.
   int64_t gx = tiles;
-  if (!a.conv) {
+  if (bn == 256) {
     const int64_t z = (int64_t)a.batch * a.heads;
     gx = std::min<int64_t>(tiles, std::max<int64_t>(1, (cu_count() + z - 1) / z));
   }

@@ -125,6 +125,14 @@ hipError_t launch_ew_fast(int dtype, const EwArgs& a, hipStream_t st);
 // per-tile partial layouts of the terminal finishers follow them.
 constexpr int kGemmTileN = 256;
 constexpr int kConvTileN = 128;
+// A bf16 conv GEMM whose chain is exactly (channel bias, ReLU) ending in an
+// average pool, with C a multiple of 64 and at least 256 positions per image,
+// runs on the persistent 256 x 256 kernel (column tiles of 256 positions);
+// other conv GEMMs on the 256 x kConvTileN one.
+bool conv_bias_relu_gap_wide(int dtype, int64_t C, int64_t PQ, const EpiDev& epi, bool gap,
+                             int pool);
+int64_t conv_gemm_tile_n(int dtype, int64_t C, int64_t PQ, const EpiDev& epi, bool gap,
+                         int pool);
 bool gemm_mfma_supported(int dtype, const GemmArgs& a);   // bf16 or fp32
 // The MFMA kernel takes B as [N, K]; a [K, N] operand (layout 1) is first
 // transposed into scratch of gemm_mfma_bt_bytes() bytes, and gemm_with_bt()

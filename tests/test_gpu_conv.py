@@ -13,9 +13,13 @@ pytestmark = pytest.mark.gpu
 if not torch.cuda.is_available():
     pytest.skip("no GPU", allow_module_level=True)
 
+# (bf16 with C % 64 == 0 and at least 256 positions per image takes the
+# persistent 256 x 256 kernel: C=64 and C=128 below, ragged in channels and in
+# position tiles that straddle images)
 CASES = [dict(N=3, C=32, H=20, W=20, K=40), dict(N=2, C=64, H=16, W=16, K=300),
          dict(N=2, C=32, H=31, W=31, K=64, stride=2), dict(N=1, C=96, H=24, W=24, K=256),
-         dict(N=2, C=8, H=9, W=7, K=5)]
+         dict(N=2, C=8, H=9, W=7, K=5), dict(N=3, C=64, H=20, W=20, K=40),
+         dict(N=2, C=128, H=20, W=20, K=264)]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
