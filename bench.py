@@ -57,10 +57,10 @@ def launch_names(mod):
             if fin:
                 seq.append(ops[-1].lower() + "_finish_kernel")
             names += seq
-        elif s["family"] == "CONV" and n >= 3:
-            names += ["pack_nhwc_kernel", "pack_krsc_kernel",
+        elif s["family"] == "CONV" and n >= 2:
+            names += ["pack_nhwc_kernel (+ weight repack)",
                       "gemm_mfma_kernel (conv: " + ",".join(ops) + ")"]
-            names += ["gap_finish_kernel"] * (n - 3)
+            names += ["gap_finish_kernel"] * (n - 2)
         elif s["family"] == "ATTN":
             names += ["attn_fwd_kernel (" + ",".join(ops) + ")"] * n
         else:

@@ -178,7 +178,7 @@ int impl_launches(const Plan& p, const Subkernel& sk, int impl) {
     return 1 + (sk.gemm.ln ? 1 : 0) + (transpose ? 1 : 0) +
            (sk.gemm.terminal != TERM_NONE ? 1 : 0);
   }
-  if (sk.family == MK_FAM_CONV && use_conv_mfma(p, sk, impl)) return sk.conv.gap ? 4 : 3;
+  if (sk.family == MK_FAM_CONV && use_conv_mfma(p, sk, impl)) return sk.conv.gap ? 3 : 2;
   return 1;
 }
 
@@ -358,9 +358,8 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       char* xp = (char*)scratch;
       char* wp = xp + cs.xp_bytes;
       float* part = (float*)(wp + cs.wp_bytes);
-      mk_status s = hip_check(timed([&] { return launch_pack_nhwc(dt, a, xp, st); }), "pack nhwc");
-      if (s != MK_OK) return s;
-      s = hip_check(timed([&] { return launch_pack_krsc(dt, a, wp, st); }), "pack krsc");
+      mk_status s =
+          hip_check(timed([&] { return launch_conv_pack(dt, a, xp, wp, st); }), "conv pack");
       if (s != MK_OK) return s;
       const GemmArgs g = conv_gemm_args(a, xp, wp, part);
       s = hip_check(timed([&] { return launch_gemm_mfma(dt, g, st); }), "conv gemm");

@@ -16,6 +16,27 @@ namespace mk {
 
 namespace {
 
+template <typename T>
+struct KrscArgs {
+  const T* w;
+  T* wp;
+  int64_t K, R, S;
+};
+
+// w [K][C][R][S] -> wp [K][R][S][C], done by the workgroups past the last
+// image of the input-packing grid (one launch packs both operands): workgroup
+// b of nb takes elements b*256*8 + t, stepping by 256, for 8 steps, and the
+// rest in grid-stride order.
+template <typename T>
+__device__ __forceinline__ void pack_krsc_part(const T* w, T* wp, int64_t K, int64_t C, int64_t R,
+                                               int64_t S, int64_t b, int64_t nb) {
+  const int64_t total = K * R * S * C;
+  for (int64_t i = b * 256 + threadIdx.x; i < total; i += nb * 256) {
+    const int64_t c = i % C, s = (i / C) % S, r = (i / (C * S)) % R, k = i / (C * S * R);
+    wp[i] = w[((k * C + c) * R + r) * S + s];
+  }
+}
+
 // x [N][C][H][W] -> xp [N][H+2pad][W+2pad][C], zero border.
 //
 // Row form (W <= 64, rows of whole 16-byte chunks): one workgroup per (padded
@@ -23,10 +44,18 @@ namespace {
 // of W values, read in 16-byte chunks; the tile is transposed in LDS and the
 // padded row written as 16-byte channel chunks, border positions as zeros.
 template <typename T>
-__global__ __launch_bounds__(256) void pack_nhwc_rows_kernel(const T* x, T* xp, int64_t C,
-                                                             int64_t H, int64_t W, int64_t pad) {
+__global__ __launch_bounds__(256) void pack_nhwc_rows_kernel(const T* x, T* xp, int64_t N,
+                                                             int64_t C, int64_t H, int64_t W,
+                                                             int64_t pad, KrscArgs<T> kw) {
   constexpr int E = 16 / (int)sizeof(T);
   __shared__ __attribute__((aligned(16))) T tile[64][64 + E];   // [w][channel]
+  if (blockIdx.z >= N) {
+    const int64_t per = (int64_t)gridDim.x * gridDim.y;
+    pack_krsc_part(kw.w, kw.wp, kw.K, C, kw.R, kw.S,
+                   (blockIdx.z - N) * per + (int64_t)blockIdx.y * gridDim.x + blockIdx.x,
+                   (gridDim.z - N) * per);
+    return;
+  }
   const int64_t Hp = H + 2 * pad, Wp = W + 2 * pad;
   const int64_t hp = blockIdx.x, c0 = (int64_t)blockIdx.y * 64, n = blockIdx.z;
   const int64_t h = hp - pad;
@@ -61,10 +90,18 @@ __global__ __launch_bounds__(256) void pack_nhwc_rows_kernel(const T* x, T* xp, 
 // General form: one workgroup per (64 padded positions, 64 channels, image),
 // one element per thread on the read side.
 template <typename T>
-__global__ __launch_bounds__(256) void pack_nhwc_kernel(const T* x, T* xp, int64_t C, int64_t H,
-                                                        int64_t W, int64_t pad) {
+__global__ __launch_bounds__(256) void pack_nhwc_kernel(const T* x, T* xp, int64_t N, int64_t C,
+                                                        int64_t H, int64_t W, int64_t pad,
+                                                        KrscArgs<T> kw) {
   constexpr int E = 16 / (int)sizeof(T);
   __shared__ __attribute__((aligned(16))) T tile[64][64 + E];
+  if (blockIdx.z >= N) {
+    const int64_t per = (int64_t)gridDim.x * gridDim.y;
+    pack_krsc_part(kw.w, kw.wp, kw.K, C, kw.R, kw.S,
+                   (blockIdx.z - N) * per + (int64_t)blockIdx.y * gridDim.x + blockIdx.x,
+                   (gridDim.z - N) * per);
+    return;
+  }
   const int64_t Hp = H + 2 * pad, Wp = W + 2 * pad, HWp = Hp * Wp;
   const int64_t pos0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64, n = blockIdx.z;
   const int t = threadIdx.x;
@@ -89,17 +126,6 @@ __global__ __launch_bounds__(256) void pack_nhwc_kernel(const T* x, T* xp, int64
   }
 }
 
-// w [K][C][R][S] -> wp [K][R][S][C].
-template <typename T>
-__global__ void pack_krsc_kernel(const T* w, T* wp, int64_t K, int64_t C, int64_t R, int64_t S) {
-  const int64_t total = K * R * S * C;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t c = i % C, s = (i / C) % S, r = (i / (C * S)) % R, k = i / (C * S * R);
-    wp[i] = w[((k * C + c) * R + r) * S + s];
-  }
-}
-
 // out[n][k] = the pool of image n from the partials of the position tiles
 // that cover it, combined in tile order (sum, or max for GMP), then finished
 // (mean over PQ, or sign(S)|S|^(1/p) for LPPOOL).  Partial (tile t, slot)
@@ -112,8 +138,11 @@ __global__ void gap_finish_kernel(const float* partial, int64_t N, int64_t K, in
   const int64_t n = i / K, k = i % K;
   const int64_t t0 = (n * PQ) / tile, t1 = ((n + 1) * PQ - 1) / tile;
   float s = pool_id(kind);
+  // A tile that starts before image n holds it in its second slot.  The
+  // loads are independent: unrolled, several are in flight at once.
+#pragma unroll 4
   for (int64_t t = t0; t <= t1; ++t) {
-    const int64_t slot = n - (t * tile) / PQ;
+    const int64_t slot = t * tile < n * PQ ? 1 : 0;
     s = pool_comb(kind, s, partial[(t * 2 + slot) * K + k]);
   }
   st<T>(out, i, pool_out(kind, p, s, (float)PQ));
@@ -147,36 +176,36 @@ ConvScratch conv_mfma_scratch(int dtype, const ConvArgs& a) {
   return s;
 }
 
+// Workgroups for the weight repack appended to the input-packing grid: whole
+// z slices of the grid, about one workgroup per 2048 weights.
+static unsigned krsc_slices(const ConvArgs& a, int64_t per_slice) {
+  const int64_t blocks = (a.K * a.R * a.S * a.C + 2047) / 2048;
+  return (unsigned)std::max<int64_t>(1, (blocks + per_slice - 1) / per_slice);
+}
+
 template <typename T>
-static void launch_pack_nhwc_t(const ConvArgs& a, void* xp, hipStream_t st) {
+static void launch_pack_t(const ConvArgs& a, void* xp, void* wp, hipStream_t st) {
   constexpr int E = 16 / (int)sizeof(T);
   const int64_t Hp = a.H + 2 * a.pad, HWp = Hp * (a.W + 2 * a.pad);
   const unsigned cb = (unsigned)((a.C + 63) / 64);
-  if (a.W <= 64 && a.W % E == 0 && (uintptr_t)a.x % 16 == 0)
-    hipLaunchKernelGGL(pack_nhwc_rows_kernel<T>, dim3((unsigned)Hp, cb, (unsigned)a.N), dim3(256),
-                       0, st, (const T*)a.x, (T*)xp, a.C, a.H, a.W, a.pad);
-  else
-    hipLaunchKernelGGL(pack_nhwc_kernel<T>, dim3((unsigned)((HWp + 63) / 64), cb, (unsigned)a.N),
-                       dim3(256), 0, st, (const T*)a.x, (T*)xp, a.C, a.H, a.W, a.pad);
+  const KrscArgs<T> kw{(const T*)a.w, (T*)wp, a.K, a.R, a.S};
+  if (a.W <= 64 && a.W % E == 0 && (uintptr_t)a.x % 16 == 0) {
+    const unsigned z = (unsigned)a.N + krsc_slices(a, Hp * cb);
+    hipLaunchKernelGGL(pack_nhwc_rows_kernel<T>, dim3((unsigned)Hp, cb, z), dim3(256), 0, st,
+                       (const T*)a.x, (T*)xp, a.N, a.C, a.H, a.W, a.pad, kw);
+  } else {
+    const unsigned gx = (unsigned)((HWp + 63) / 64);
+    const unsigned z = (unsigned)a.N + krsc_slices(a, (int64_t)gx * cb);
+    hipLaunchKernelGGL(pack_nhwc_kernel<T>, dim3(gx, cb, z), dim3(256), 0, st, (const T*)a.x,
+                       (T*)xp, a.N, a.C, a.H, a.W, a.pad, kw);
+  }
 }
 
-hipError_t launch_pack_nhwc(int dtype, const ConvArgs& a, void* xp, hipStream_t st) {
+hipError_t launch_conv_pack(int dtype, const ConvArgs& a, void* xp, void* wp, hipStream_t st) {
   if (dtype == MK_BF16)
-    launch_pack_nhwc_t<bf16>(a, xp, st);
+    launch_pack_t<bf16>(a, xp, wp, st);
   else
-    launch_pack_nhwc_t<float>(a, xp, st);
-  return hipGetLastError();
-}
-
-hipError_t launch_pack_krsc(int dtype, const ConvArgs& a, void* wp, hipStream_t st) {
-  const int64_t total = a.K * a.R * a.S * a.C;
-  const unsigned g = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
-  if (dtype == MK_BF16)
-    hipLaunchKernelGGL(pack_krsc_kernel<bf16>, dim3(g), dim3(256), 0, st, (const bf16*)a.w,
-                       (bf16*)wp, a.K, a.C, a.R, a.S);
-  else
-    hipLaunchKernelGGL(pack_krsc_kernel<float>, dim3(g), dim3(256), 0, st, (const float*)a.w,
-                       (float*)wp, a.K, a.C, a.R, a.S);
+    launch_pack_t<float>(a, xp, wp, st);
   return hipGetLastError();
 }
 
@@ -215,12 +244,14 @@ GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float
 hipError_t launch_gap_finish(int dtype, const ConvArgs& a, const float* partial, hipStream_t st) {
   const int64_t total = a.N * a.K;
   const int64_t tn = conv_gemm_tile_n(dtype, a.C, a.P * a.Q, a.epi, a.gap, a.pool);
-  const dim3 grid((unsigned)((total + 255) / 256));
+  // One wave per workgroup: N*K outputs are few (16384 for 64 images of 256
+  // channels), so small workgroups spread them over every CU.
+  const dim3 grid((unsigned)((total + 63) / 64));
   if (dtype == MK_BF16)
-    hipLaunchKernelGGL(gap_finish_kernel<bf16>, grid, dim3(256), 0, st, partial, a.N, a.K,
+    hipLaunchKernelGGL(gap_finish_kernel<bf16>, grid, dim3(64), 0, st, partial, a.N, a.K,
                        a.P * a.Q, tn, (int)a.pool, a.pool_p, (bf16*)a.y);
   else
-    hipLaunchKernelGGL(gap_finish_kernel<float>, grid, dim3(256), 0, st, partial, a.N, a.K,
+    hipLaunchKernelGGL(gap_finish_kernel<float>, grid, dim3(64), 0, st, partial, a.N, a.K,
                        a.P * a.Q, tn, (int)a.pool, a.pool_p, (float*)a.y);
   return hipGetLastError();
 }

@@ -148,7 +148,7 @@ hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st);
 constexpr int kSmallGemmTiles = 64;
 int64_t gemm_mfma_tile_n(int dtype, const GemmArgs& a);
 hipError_t launch_gemm_small(int dtype, const GemmArgs& a, hipStream_t st);
-// Implicit-GEMM conv: pack_nhwc (x -> zero-padded NHWC), pack_krsc (w ->
+// Implicit-GEMM conv: one packing launch (x -> zero-padded NHWC, w ->
 // [K][R][S][C]), the GEMM kernel in conv mode, and for a fused GAP the
 // finisher over per-tile partials.
 struct ConvScratch {
@@ -156,8 +156,7 @@ struct ConvScratch {
 };
 bool conv_mfma_supported(int dtype, const ConvArgs& a);
 ConvScratch conv_mfma_scratch(int dtype, const ConvArgs& a);
-hipError_t launch_pack_nhwc(int dtype, const ConvArgs& a, void* xp, hipStream_t st);
-hipError_t launch_pack_krsc(int dtype, const ConvArgs& a, void* wp, hipStream_t st);
+hipError_t launch_conv_pack(int dtype, const ConvArgs& a, void* xp, void* wp, hipStream_t st);
 GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float* partial);
 hipError_t launch_gap_finish(int dtype, const ConvArgs& a, const float* partial, hipStream_t st);
 bool attn_fused_supported(int dtype, const AttnArgs& a);
