@@ -20,6 +20,14 @@ __device__ __forceinline__ bf16 f2bf(float f) {
   return __builtin_bit_cast(bf16, h);
 }
 
+// Two values rounded to bf16 and packed (lo in the low half): one packed
+// conversion instruction.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
+}
+
 template <typename T> __device__ __forceinline__ float ld(const T* p, int64_t i);
 template <> __device__ __forceinline__ float ld<float>(const float* p, int64_t i) { return p[i]; }
 template <> __device__ __forceinline__ float ld<bf16>(const bf16* p, int64_t i) {
@@ -124,10 +132,10 @@ template <typename T>
 __device__ __forceinline__ void st8(T* p, const float (&v)[8]) {
   if constexpr (sizeof(T) == 2) {
     uint4 o;
-    o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-    o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-    o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
-    o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+    o.x = pack2_bf16(v[0], v[1]);
+    o.y = pack2_bf16(v[2], v[3]);
+    o.z = pack2_bf16(v[4], v[5]);
+    o.w = pack2_bf16(v[6], v[7]);
     *(uint4*)p = o;
   } else {
     *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);

@@ -22,6 +22,8 @@
 //    dh d0 + 4*(j%4) hands every lane 4 consecutive keys of one dh column.
 //  * exp is exp2 with log2(e) folded into the score scale; key blocks above
 //    a wave's diagonal are skipped.
+#include <type_traits>
+
 #include "dev.hpp"
 
 namespace mk {
@@ -33,6 +35,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 namespace {
 
 constexpr int BQ = 128, BKV = 64, kThreads = 256;
+constexpr float kLazy = 8.0f;   // log2 headroom of the running softmax reference
 constexpr int kXcds = 8;
 constexpr uint32_t kOob = 0x80000000u;
 
@@ -59,9 +62,6 @@ __device__ __forceinline__ int sigma(int i) {
   return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1);
 }
 
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
-}
 
 template <int N>
 __device__ __forceinline__ void wait_vm() {
@@ -119,6 +119,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
     }
   }
 
+  const int Si = (int)S, wq0i = (int)wq0, qii = (int)qi;
   const int nkb = (int)((S + BKV - 1) / BKV);
   const int n_kv = CAUSAL ? min(nkb, (int)((q0 + BQ + BKV - 1) / BKV)) : nkb;
 
@@ -135,13 +136,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
     vchunk[q] = p % (DH / 8);
     kchunk[q] = vchunk[q] ^ (sigma(krow_of[q]) & 7);
   }
-  // One block of K or V into dst.
-  auto issue = [&](__amdgpu_buffer_rsrc_t src, const int (&chunk)[KLOADS], int j, char* dst) {
+  // Byte offsets of this lane's rows within a block (32-bit: the sequence's
+  // rows span less than 2 GB) and the wave's LDS chunks (wave-uniform).
+  const uint32_t rowb = (uint32_t)(ld3 * 2);
+  uint32_t koff[KLOADS], voff[KLOADS];
+#pragma unroll
+  for (int q = 0; q < KLOADS; ++q) {
+    koff[q] = (uint32_t)krow_of[q] * rowb + kchunk[q] * 16;
+    voff[q] = (uint32_t)krow_of[q] * rowb + vchunk[q] * 16;
+  }
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  // One block of K or V into dst (rows past the sequence read zeros).
+  auto issue = [&](__amdgpu_buffer_rsrc_t src, const uint32_t (&off0)[KLOADS], int j, char* dst) {
+    const int krem = (int)min<int64_t>(S - (int64_t)j * BKV, BKV);   // keys left in the block
+    const uint32_t jb = (uint32_t)j * BKV * rowb;
 #pragma unroll
     for (int q = 0; q < KLOADS; ++q) {
-      const int64_t key = (int64_t)j * BKV + krow_of[q];
-      const uint32_t off = key < S ? (uint32_t)(key * ld3 * 2 + chunk[q] * 16) : kOob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * 4 + w) * 1024), 16,
+      const uint32_t off = krow_of[q] < krem ? off0[q] + jb : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * 4 + wu) * 1024), 16,
                                                (int)off, 0, 0, 0);
     }
   };
@@ -158,22 +170,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
   const float sl2 = a.scale * 1.4426950408889634f;   // scale * log2(e)
 
-  issue(ksrc, kchunk, 0, smem);
-  issue(vsrc, vchunk, 0, smem + KBYTES);
+  issue(ksrc, koff, 0, smem);
+  issue(vsrc, voff, 0, smem + KBYTES);
 
-  for (int j = 0; j < n_kv; ++j) {
-    char* cur = smem + (j & 1) * STAGE;
-    char* nxt = smem + ((j + 1) & 1) * STAGE;
+  // Block j uses stage j % 2; the loop body is instantiated for both
+  // parities so that the stage base is a constant offset of the LDS reads.
+  auto block = [&](int j, auto PAR) {
+    constexpr int par = decltype(PAR)::value;
+    char* cur = smem + par * STAGE;
+    char* nxt = smem + (1 - par) * STAGE;
     // Block j has landed (this wave's loads); the barrier makes every wave's
     // loads visible and guarantees block j-1's slot is no longer read.
     wait_vm<0>();
     __builtin_amdgcn_s_barrier();
     if (j + 1 < n_kv) {
-      issue(ksrc, kchunk, j + 1, nxt);
-      issue(vsrc, vchunk, j + 1, nxt + KBYTES);
+      issue(ksrc, koff, j + 1, nxt);
+      issue(vsrc, voff, j + 1, nxt + KBYTES);
     }
-    const int64_t kv0 = (int64_t)j * BKV;
-    const bool active = !CAUSAL || kv0 <= wq0 + 31;
+    const int kv0 = j * BKV;                       // (sequences are below 2^31 rows)
+    const bool active = !CAUSAL || kv0 <= wq0i + 31;
     if (active) {
       // S^T for the block: two 32-key tiles.
       f32x16 sacc[2];
@@ -192,10 +207,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
       // Register r of tile kt holds key kv0 + kt*32 + (r/8)*16 + lh*8 + r%8
       // for query qi.  Only blocks that cross the wave's diagonal or the end
       // of the sequence need the mask.
-      const bool need_mask = (CAUSAL && kv0 + BKV - 1 > wq0) || kv0 + BKV > S;
+      const bool need_mask = (CAUSAL && kv0 + BKV - 1 > wq0i) || kv0 + BKV > Si;
       if (need_mask) {
-        const int qrel = (int)(qi - kv0);           // keys kv0 + k with k > qrel are masked
-        const int kmax = (int)min<int64_t>(BKV, S - kv0);
+        const int qrel = qii - kv0;                 // keys kv0 + k with k > qrel are masked
+        const int kmax = min(BKV, Si - kv0);
         const int lim = CAUSAL ? min(a.causal == 2 ? qrel - 1 : qrel, kmax - 1) : kmax - 1;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
@@ -211,7 +226,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sacc[kt][r]);
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * sl2;
-      const float m_new = fmaxf(m_run, mloc);
+      // The reference m_run moves only when the block's max exceeds it by
+      // more than kLazy (log2 units): probabilities stay below 2^kLazy, and
+      // the rescale of O and l (exact either way: both carry the same
+      // reference) is skipped for most blocks.
+      const float m_new = mloc > m_run + kLazy ? mloc : m_run;
       const float mneg = m_new == -INFINITY ? 0.f : -m_new;
       const float alpha = __builtin_amdgcn_exp2f(m_run + mneg);   // 0 on the first block
       float lsum = 0.f;
@@ -223,7 +242,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
           const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[kt][r], sl2, mneg));
           const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[kt][r + 1], sl2, mneg));
           lsum += p0 + p1;
-          pp[kt][r >> 1] = pack_bf16(p0, p1);
+          pp[kt][r >> 1] = pack2_bf16(p0, p1);
         }
       l_run = l_run * alpha + lsum;
       m_run = m_new;
@@ -253,6 +272,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
         }
       }
     }
+  };
+  for (int j = 0; j < n_kv; j += 2) {
+    block(j, std::integral_constant<int, 0>{});
+    if (j + 1 < n_kv) block(j + 1, std::integral_constant<int, 1>{});
   }
   wait_vm<0>();
   __syncthreads();

@@ -877,7 +877,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
           u32x4 o;
 #pragma unroll
           for (int k = 0; k < 4; ++k)
-            o[k] = (uint32_t)f2bf(v[2 * k]) | ((uint32_t)f2bf(v[2 * k + 1]) << 16);
+            o[k] = pack2_bf16(v[2 * k], v[2 * k + 1]);
           __builtin_amdgcn_raw_buffer_store_b128(o, rcst, (int)roff, 0, 0);
         } else {
 #pragma unroll

@@ -60,3 +60,22 @@ def test_mask_off_by_one_mutant_is_caught():
     assert not rep["pass"]
     rep, *_ = run_parity(module, g, impls={0: mk.IMPL_SIMPLE})
     assert rep["pass"], describe(rep)
+
+
+def test_fused_attention_growing_scores():
+    """Keys whose scale grows along the sequence (and a few large spikes), so
+    that the running maximum of a query's scores rises by many units after
+    the first key blocks: the fused kernel moves its softmax reference (and
+    rescales the partial output) only when the maximum exceeds it by more
+    than a fixed margin, and must still match the oracle."""
+    from paper_2607_20501_amd import inputs
+    B, S, H, dh = 1, 1024, 2, 128
+    module = attn_module(B, S, H, dh, True)
+    x = inputs.bf16_bits_to_f32(inputs.make_inputs(module, 3)[0]).reshape(B * S, 3 * H * dh)
+    key = np.arange(B * S) % S
+    ramp = (1.0 + 6.0 * key / S).astype(np.float32)[:, None]
+    x[:, H * dh:2 * H * dh] *= ramp                       # K grows along the keys
+    x[[100, 400, 700, 900], H * dh:2 * H * dh] *= 4.0     # and jumps at a few keys
+    bits = (x.astype(np.float32).view(np.uint32) + 0x7FFF + ((x.view(np.uint32) >> 16) & 1)) >> 16
+    rep, *_ = run_parity(module, [0] * len(module["ops"]), host=[bits.astype(np.uint16).ravel()])
+    assert rep["pass"], describe(rep)
