@@ -49,10 +49,10 @@ __global__ __launch_bounds__(256) void ew_fast_kernel(EwFastArgs a) {
       epi_apply8<T>(a.full.epi, v[j], row, col, ch, 8, i0, true);
       if constexpr (sizeof(T) == 2) {
         uint4 o;
-        o.x = (uint32_t)f2bf(v[j][0]) | ((uint32_t)f2bf(v[j][1]) << 16);
-        o.y = (uint32_t)f2bf(v[j][2]) | ((uint32_t)f2bf(v[j][3]) << 16);
-        o.z = (uint32_t)f2bf(v[j][4]) | ((uint32_t)f2bf(v[j][5]) << 16);
-        o.w = (uint32_t)f2bf(v[j][6]) | ((uint32_t)f2bf(v[j][7]) << 16);
+        o.x = pack2_bf16(v[j][0], v[j][1]);
+        o.y = pack2_bf16(v[j][2], v[j][3]);
+        o.z = pack2_bf16(v[j][4], v[j][5]);
+        o.w = pack2_bf16(v[j][6], v[j][7]);
         *(uint4*)(y + (int64_t)i0) = o;
       } else {
         *(float4*)(y + (int64_t)i0) = make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
