@@ -4,6 +4,8 @@
 // subtracted, App. D), LayerNorm (mean, then the biased variance of the
 // centred values; App. H.2 / App. I.2).  Each value is read from HBM once and
 // each output written once.
+#include <algorithm>
+
 #include "dev.hpp"
 
 namespace mk {
@@ -135,11 +137,124 @@ __global__ __launch_bounds__(64) void row_wave_kernel(RowArgs a) {
     }
 }
 
+// LayerNorm over rows with persistent waves: gamma and beta of the lane's
+// columns stay in registers across rows, and the next row is requested
+// before the current one is reduced (two row buffers in alternation), so a
+// wave keeps a row of loads in flight while it computes.  Rows past the end
+// and columns past L read valid memory (clamped) and are not stored.
+template <typename T, int NV>
+__global__ __launch_bounds__(64) void ln_rows_kernel(RowArgs a) {
+  constexpr int E = kEpv<T>;
+  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+  const int lane = threadIdx.x & 63;
+  const int64_t L = a.len, rows = a.rows, step = gridDim.x;
+  const T* X = (const T*)a.x;
+  T* Y = (T*)a.y;
+  bool ok[NV];
+  int64_t col[NV];
+  u32x4_t g[NV], be[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    col[i] = (int64_t)(i * 64 + lane) * E;
+    ok[i] = col[i] < L;
+    const int64_t cc = ok[i] ? col[i] : 0;
+    g[i] = *(const u32x4_t*)((const T*)a.gamma + cc);
+    be[i] = *(const u32x4_t*)((const T*)a.beta + cc);
+  }
+  auto load_row = [&](int64_t r, u32x4_t (&dst)[NV]) {
+    const int64_t rr = r < rows ? r : rows - 1;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) dst[i] = *(const u32x4_t*)(X + rr * L + (ok[i] ? col[i] : 0));
+  };
+  auto unpack = [&](const u32x4_t& w, float (&out)[E]) {
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        out[2 * k] = __uint_as_float(w[k] << 16);
+        out[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) out[k] = __uint_as_float(w[k]);
+    }
+  };
+  // (The row stays packed: each pass unpacks it again, which keeps the
+  // register count at two occupancy levels above float copies.)
+  auto do_row = [&](int64_t r, const u32x4_t (&src)[NV]) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      float v[E];
+      unpack(src[i], v);
+#pragma unroll
+      for (int k = 0; k < E; ++k) s += ok[i] ? v[k] : 0.f;
+    }
+    const float mu = warp_sum(s) / (float)L;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      float v[E];
+      unpack(src[i], v);
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        const float d = v[k] - mu;
+        q += ok[i] ? d * d : 0.f;
+      }
+    }
+    const float rstd = rsqrtf(warp_sum(q) / (float)L + a.eps);
+    if (r >= rows) return;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      if (!ok[i]) continue;
+      float v[E], gg[E], bb[E];
+      // gamma and beta are unpacked per row: an opaque copy keeps the
+      // compiler from hoisting 2 * NV * E floats out of the row loop.
+      u32x4_t gi = g[i], bi = be[i];
+      asm volatile("" : "+v"(gi), "+v"(bi));
+      unpack(src[i], v);
+      unpack(gi, gg);
+      unpack(bi, bb);
+#pragma unroll
+      for (int k = 0; k < E; ++k) v[k] = (v[k] - mu) * rstd * gg[k] + bb[k];
+      st_vec<T>(Y + r * L + col[i], v);
+    }
+  };
+  int64_t r = blockIdx.x;
+  u32x4_t xa[NV], xb[NV];
+  load_row(r, xa);
+  for (; r < rows; r += 2 * step) {
+    load_row(r + step, xb);
+    do_row(r, xa);
+    if (r + step >= rows) break;
+    load_row(r + 2 * step, xa);
+    do_row(r + step, xb);
+  }
+}
+
+// Persistent LayerNorm waves: about eight per CU.
+static int ln_waves() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+    n = 256;
+  return 8 * n;
+}
+
 template <typename T>
 hipError_t launch_row_wave_t(const RowArgs& a, hipStream_t st) {
   constexpr int E = kEpv<T>;
   const int64_t nv = (a.len + 64 * E - 1) / (64 * E);
   const dim3 grid((unsigned)a.rows), block(64);
+  if (a.op == MK_OP_LAYERNORM) {
+    const dim3 pg((unsigned)std::min<int64_t>(a.rows, ln_waves()));
+    switch (nv) {
+      case 1: hipLaunchKernelGGL((ln_rows_kernel<T, 1>), pg, block, 0, st, a); break;
+      case 2: hipLaunchKernelGGL((ln_rows_kernel<T, 2>), pg, block, 0, st, a); break;
+      case 3: case 4: hipLaunchKernelGGL((ln_rows_kernel<T, 4>), pg, block, 0, st, a); break;
+      default: hipLaunchKernelGGL((ln_rows_kernel<T, 8>), pg, block, 0, st, a); break;
+    }
+    return hipGetLastError();
+  }
   switch (nv) {
     case 1: hipLaunchKernelGGL((row_wave_kernel<T, 1>), grid, block, 0, st, a); break;
     case 2: hipLaunchKernelGGL((row_wave_kernel<T, 2>), grid, block, 0, st, a); break;
