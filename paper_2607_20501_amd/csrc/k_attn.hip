@@ -190,19 +190,21 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
     const int kv0 = j * BKV;                       // (sequences are below 2^31 rows)
     const bool active = !CAUSAL || kv0 <= wq0i + 31;
     if (active) {
-      // S^T for the block: two 32-key tiles.
+      // S^T for the block: two 32-key tiles, their MFMA chains interleaved
+      // (each MFMA's successor on the same accumulator waits for it).
       f32x16 sacc[2];
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[kt][r] = 0.f;
-        const char* krow = cur + (kt * 32 + sigma(lr)) * KROW;
 #pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
+      for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+          const char* krow = cur + (kt * 32 + sigma(lr)) * KROW;
           const bf16x8 kf = *(const bf16x8*)(krow + (((ks * 2 + lh) ^ (lr & 7)) * 16));
           sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sacc[kt], 0, 0, 0);
         }
-      }
       // Scores, mask, running max, in units of log2: s * scale * log2(e).
       // Register r of tile kt holds key kv0 + kt*32 + (r/8)*16 + lh*8 + r%8
       // for query qi.  Only blocks that cross the wave's diagonal or the end
