@@ -55,7 +55,12 @@ def launch_names(mod):
                 seq.append("transpose_b_kernel")
             seq.append("gemm_mfma_kernel (" + ",".join(ops) + ")")
             if fin:
-                seq.append(ops[-1].lower() + "_finish_kernel")
+                # (a softmax over rows one wave holds runs as a row pass over
+                # the stored values; otherwise a finisher over partials)
+                row_pass = ops[-1] == "SOFTMAX" and s.get("out_shape", [0])[-1] * (
+                    2 if mod.desc["dtype"] == "bf16" else 4) <= 8192
+                seq.append("row_wave_kernel (softmax)" if row_pass
+                           else ops[-1].lower() + "_finish_kernel")
             names += seq
         elif s["family"] == "CONV" and n >= 2:
             names += ["pack_nhwc_kernel (+ weight repack)",

@@ -69,9 +69,12 @@ __device__ __forceinline__ float gelu_erf(float x) {
 // x * sigmoid(2u) with u = sqrt(2/pi) (x + 0.044715 x^3).  exp(-2u) is taken
 // as 2^(-2u log2 e); the reciprocal is the hardware one (1 ulp): for very
 // negative x it sees +inf and gives 0.
+// The exponent -2u log2 e = x (k0 + k1 x^2) with k0 = -2 sqrt(2/pi) log2 e,
+// k1 = 0.044715 k0: one multiply, one FMA, one multiply.
 __device__ __forceinline__ float gelu_tanh(float x) {
-  const float c2l = 2.3022081983f;   // 2 sqrt(2 / pi) log2(e)
-  const float e = __builtin_amdgcn_exp2f(-c2l * fmaf(0.044715f * x, x * x, x));
+  const float k0 = -2.3022081983f;           // -2 sqrt(2 / pi) log2(e)
+  const float k1 = -0.10294324f;             // 0.044715 k0
+  const float e = __builtin_amdgcn_exp2f(x * fmaf(k1, x * x, k0));
   return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
@@ -246,6 +249,26 @@ __device__ __forceinline__ Moments mom_comb(const Moments& a, const Moments& b) 
 }
 __device__ __forceinline__ Moments mom_shfl_xor(const Moments& a, int o) {
   return {__shfl_xor(a.n, o, 64), __shfl_xor(a.mean, o, 64), __shfl_xor(a.m2, o, 64)};
+}
+
+// The value of lane (this lane ^ O), O = 8, 16 or 32, by VALU lane
+// exchanges instead of an LDS permute: a DPP rotate by 8 within each 16-lane
+// row; the gfx950 swaps of odd with even 16-lane rows and of the two 32-lane
+// halves (each returns both operands after the swap; a lane takes the half
+// that came from its partner).
+template <int O>
+__device__ __forceinline__ float lane_xor(float x) {
+  const int b = __builtin_bit_cast(int, x);
+  if constexpr (O == 8) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, b, 0x128, 0xF, 0xF, false));
+  } else if constexpr (O == 16) {
+    const auto p = __builtin_amdgcn_permlane16_swap((unsigned)b, (unsigned)b, false, false);
+    return __builtin_bit_cast(float, (threadIdx.x & 16) ? p[0] : p[1]);
+  } else {
+    static_assert(O == 32, "lane_xor: 8, 16 or 32");
+    const auto p = __builtin_amdgcn_permlane32_swap((unsigned)b, (unsigned)b, false, false);
+    return __builtin_bit_cast(float, (threadIdx.x & 32) ? p[0] : p[1]);
+  }
 }
 
 __device__ __forceinline__ float warp_sum(float v) {

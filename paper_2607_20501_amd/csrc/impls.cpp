@@ -317,12 +317,34 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       }
       a.partial = (float*)sc;
       a.n_tiles = gs.n_tiles;
+      // A softmax over rows one wave can hold: the GEMM writes the chain's
+      // values (as stored, i.e. rounded) and a one-wave-per-row softmax reads
+      // them back in place (max, exp, sum, normalise; the same HBM traffic as
+      // the partials' finisher, and no softmax work in the GEMM epilogue).
+      // Otherwise the epilogue emits per-tile partials for the finisher.
+      RowArgs rs{};
+      bool row_softmax = false;
+      if (gs.mfma && g.terminal == TERM_SOFTMAX && g.batch * g.heads == 1 && g.ldc == g.N) {
+        char* c0 = (char*)out + g.c_off * elem_size(p.dtype);
+        rs.x = c0;
+        rs.y = c0;
+        rs.rows = g.M;
+        rs.len = g.N;
+        rs.op = MK_OP_SOFTMAX;
+        rs.pre.last = rs.pre.S = rs.pre.C = rs.pre.HW = 1;
+        rs.n2 = 1;
+        row_softmax = row_wave_supported(dt, rs);
+      }
+      if (row_softmax) a.terminal = TERM_NONE;
       mk_status s = hip_check(timed([&] {
                                 return gs.mfma ? launch_gemm_mfma(dt, a, st)
                                                : launch_gemm_simple(dt, a, st);
                               }),
                               "gemm");
       if (s != MK_OK) return s;
+      if (row_softmax)
+        return hip_check(timed([&] { return launch_row(dt, rs, st, MK_IMPL_TUNED); }),
+                         "softmax rows");
       if (g.terminal == TERM_ROWSUM)
         return hip_check(timed([&] {
                            return launch_rowsum_finish(dt, a.partial, g.M, a.n_tiles, out, st);

@@ -77,12 +77,15 @@ constexpr int kSigNone = 2;              // no chain, no terminal
 constexpr int kSigGeluErf = 3;           // exact GELU
 constexpr int kSigAdd = 4;               // residual add (operand laid out as C)
 constexpr int kSigBiasGeluTanhScaleSoftmax = 5;   // bias, tanh GELU, scale; softmax partials
+constexpr int kSigBiasGeluTanhScale = 6;          // bias, tanh GELU, scale
 
 // Terminal of a signature (-1: read at run time).
 constexpr int sig_terminal(int sig) {
   return sig == kSigBiasGeluTanhScaleSoftmax ? TERM_SOFTMAX
-         : (sig == kSigNone || sig == kSigGeluErf || sig == kSigAdd) ? TERM_NONE
-                                                                      : -1;
+         : (sig == kSigNone || sig == kSigGeluErf || sig == kSigAdd ||
+            sig == kSigBiasGeluTanhScale)
+             ? TERM_NONE
+             : -1;
 }
 constexpr int kGroupM = 8;                        // tile rows per locality group
 constexpr int kXcds = 8;
@@ -644,8 +647,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   };
   float bias_reg = load_bias_reg(tc);
   bool staged0 = false;   // this tile's stage 0 was issued during the last epilogue
-  constexpr int kEpiVmem =
-      (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd) ? 16 : 0;
+  constexpr int kEpiVmem = (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
+                            SIG == kSigBiasGeluTanhScale)
+                               ? 16
+                               : 0;
   for (;;) {
     const int64_t m0 = (int64_t)tc.tm * BM, n0 = (int64_t)tc.tn * BN;
     f32x16 acc[4][NJ];
@@ -813,7 +818,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     const int64_t img = CONV ? col0 / PQ : 0;
 
     // Compiled TERM_NONE chains store through a buffer resource over C.
-    constexpr bool kBufStore = SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd;
+    constexpr bool kBufStore = SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
+                               SIG == kSigBiasGeluTanhScale;
     const __amdgpu_buffer_rsrc_t rcst =
         make_rsrc(C, kBufStore ? a.M * a.ldc * (int64_t)sizeof(T) : 0);
     // Residual operand (laid out as C; range checked by signature selection).
@@ -822,7 +828,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
                   SIG == kSigAdd ? a.M * a.ldc * (int64_t)sizeof(T) : 0);
     // Column bias of this lane's 8 columns, once per tile.
     float bcol[8];
-    if constexpr (SIG == kSigBiasGeluTanhScaleSoftmax)
+    if constexpr (SIG == kSigBiasGeluTanhScaleSoftmax || SIG == kSigBiasGeluTanhScale)
       ld8<T>((const T*)a.epi.ptr[0] + col0, valid == 8 && vec_ok, valid, bcol);
 
     // One row of the lane: values v of columns col0 .. col0+7 of tile row
@@ -853,10 +859,11 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         }
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] += (row_ok && e < valid) ? t8[e] : 0.f;
-      } else if constexpr (SIG == kSigBiasGeluTanhScaleSoftmax) {
+      } else if constexpr (SIG == kSigBiasGeluTanhScaleSoftmax || SIG == kSigBiasGeluTanhScale) {
+        // (v arrives without alpha: alpha * acc + bias is one FMA)
         const float sc = a.epi.s[2];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = gelu_tanh(v[e] + bcol[e]) * sc;
+        for (int e = 0; e < 8; ++e) v[e] = gelu_tanh(fmaf(v[e], a.alpha, bcol[e])) * sc;
       } else if constexpr (SIG == kSigGeneric || SIG == kSigConvBiasReluGap) {
         if (a.epi.n && row_ok && valid > 0)
           epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok),
@@ -924,20 +931,24 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         if (softmax) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) m = fmaxf(m, e < valid ? v[e] : -INFINITY);
-#pragma unroll
-          for (int o = 8; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+          m = fmaxf(m, lane_xor<8>(m));
+          m = fmaxf(m, lane_xor<16>(m));
+          m = fmaxf(m, lane_xor<32>(m));
           const bool any = m != -INFINITY;
+          // exp(v - m) = 2^(v log2 e - m log2 e): one FMA and exp2
+          const float ml = any ? m * 1.4426950408889634f : 0.f;
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const float x = __expf(v[e] - m);
+            const float x = __builtin_amdgcn_exp2f(fmaf(v[e], 1.4426950408889634f, -ml));
             sum += (e < valid && any) ? x : 0.f;
           }
         } else {
 #pragma unroll
           for (int e = 0; e < 8; ++e) sum += e < valid ? v[e] : 0.f;
         }
-#pragma unroll
-        for (int o = 8; o < 64; o <<= 1) sum += __shfl_xor(sum, o, 64);
+        sum += lane_xor<8>(sum);
+        sum += lane_xor<16>(sum);
+        sum += lane_xor<32>(sum);
         if (q == 0) {
           red[(wn * 256 + lrow) * 2] = m;
           red[(wn * 256 + lrow) * 2 + 1] = sum;
@@ -958,19 +969,31 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       // The slab is rewritten next: every lane's reads of it must be done.
       __builtin_amdgcn_s_waitcnt(0xc07f);
       __builtin_amdgcn_wave_barrier();
-      // Row t of the quad is element 0 after t rotations (static indices in
-      // a loop that is not unrolled).
-#pragma unroll 1
-      for (int t = 0; t < 4; ++t) {
-        float v[8];
+      if constexpr (SIG == kSigBiasGeluTanhScaleSoftmax) {
+        // Rows unrolled (static quad indices, no rotation); alpha enters the
+        // chain's first FMA.
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          v[e] = u[e][0] * a.alpha;
-          u[e] = f32x4{u[e][1], u[e][2], u[e][3], u[e][0]};
+        for (int t = 0; t < 4; ++t) {
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = u[e][t];
+          finish_row(rowbase + i * 32 + rg * 4 + t, v, u32x4{0, 0, 0, 0}, 0.f);
         }
-        const float bt = bq[0];
-        bq = f32x4{bq[1], bq[2], bq[3], bq[0]};
-        finish_row(rowbase + i * 32 + rg * 4 + t, v, u32x4{0, 0, 0, 0}, bt);
+      } else {
+        // Row t of the quad is element 0 after t rotations (static indices
+        // in a loop that is not unrolled).
+#pragma unroll 1
+        for (int t = 0; t < 4; ++t) {
+          float v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            v[e] = u[e][0] * a.alpha;
+            u[e] = f32x4{u[e][1], u[e][2], u[e][3], u[e][0]};
+          }
+          const float bt = bq[0];
+          bq = f32x4{bq[1], bq[2], bq[3], bq[0]};
+          finish_row(rowbase + i * 32 + rg * 4 + t, v, u32x4{0, 0, 0, 0}, bt);
+        }
       }
     };
 
@@ -1003,13 +1026,15 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       for (int t = 0; t < 4; ++t) {
         float v[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = u[e][t] * a.alpha;
+        for (int e = 0; e < 8; ++e)
+          v[e] = SIG == kSigBiasGeluTanhScale ? u[e][t] : u[e][t] * a.alpha;
         finish_row(rowbase + I * 32 + rg * 4 + t, v, cur[t], 0.f);
       }
     };
     if (SIG == kSigConvBiasReluGap || (CONV && term == TERM_GAP)) {
       gap_from_acc<T, NJ, SIG == kSigConvBiasReluGap>(a, acc, m0, n0, rowbase, colbase, wn, lr, lh, pre_ch, rbias, red);
-    } else if constexpr (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd) {
+    } else if constexpr (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
+                         SIG == kSigBiasGeluTanhScale) {
       // (The softmax-partial chain keeps the rolled loop: unrolled, its
       // live values spill.)
       u32x4 ra[4], rb[4];
@@ -1202,6 +1227,9 @@ static int gemm_signature(const GemmArgs& a) {
     if (e.n == 0) return kSigNone;
     if (e.n == 1 && e.code[0] == EPI_GELU_ERF) return kSigGeluErf;
     if (e.n == 1 && e.code[0] == EPI_ADD) return kSigAdd;
+    if (e.n == 3 && e.code[0] == EPI_BIAS_COL && e.code[1] == EPI_GELU_TANH &&
+        e.code[2] == EPI_SCALE)
+      return kSigBiasGeluTanhScale;
   } else if (a.terminal == TERM_SOFTMAX && e.n == 3 && e.code[0] == EPI_BIAS_COL &&
              e.code[1] == EPI_GELU_TANH && e.code[2] == EPI_SCALE) {
     return kSigBiasGeluTanhScaleSoftmax;
@@ -1263,6 +1291,7 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
       MK_GEMM_SIG(kSigGeluErf)
       MK_GEMM_SIG(kSigAdd)
       MK_GEMM_SIG(kSigBiasGeluTanhScaleSoftmax)
+      MK_GEMM_SIG(kSigBiasGeluTanhScale)
       default:
         MK_GEMM_SIG(kSigGeneric)
 #undef MK_GEMM_SIG
