@@ -231,7 +231,84 @@ __global__ __launch_bounds__(64) void ln_rows_kernel(RowArgs a) {
   }
 }
 
-// Persistent LayerNorm waves: about eight per CU.
+// Softmax over rows (max subtracted) on persistent waves, like the LayerNorm
+// rows: the next row is requested before the current one is reduced; the
+// exponentials stay in registers between the sum and the normalisation.
+template <typename T, int NV>
+__global__ __launch_bounds__(64) void softmax_rows_kernel(RowArgs a) {
+  constexpr int E = kEpv<T>;
+  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+  const int lane = threadIdx.x & 63;
+  const int64_t L = a.len, rows = a.rows, step = gridDim.x;
+  const T* X = (const T*)a.x;
+  T* Y = (T*)a.y;
+  bool ok[NV];
+  int64_t col[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    col[i] = (int64_t)(i * 64 + lane) * E;
+    ok[i] = col[i] < L;
+  }
+  auto load_row = [&](int64_t r, u32x4_t (&dst)[NV]) {
+    const int64_t rr = r < rows ? r : rows - 1;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) dst[i] = *(const u32x4_t*)(X + rr * L + (ok[i] ? col[i] : 0));
+  };
+  auto unpack = [&](const u32x4_t& w, float (&out)[E]) {
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        out[2 * k] = __uint_as_float(w[k] << 16);
+        out[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) out[k] = __uint_as_float(w[k]);
+    }
+  };
+  auto do_row = [&](int64_t r, const u32x4_t (&src)[NV]) {
+    float e[NV][E];
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      unpack(src[i], e[i]);
+#pragma unroll
+      for (int k = 0; k < E; ++k) m = fmaxf(m, ok[i] ? e[i][k] : -INFINITY);
+    }
+    m = warp_max(m);
+    // exp(v - m) = 2^(v log2 e - m log2 e)
+    const float ml = m * 1.4426950408889634f;
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        e[i][k] = __builtin_amdgcn_exp2f(fmaf(e[i][k], 1.4426950408889634f, -ml));
+        s += ok[i] ? e[i][k] : 0.f;
+      }
+    const float inv = 1.0f / warp_sum(s);
+    if (r >= rows) return;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      if (!ok[i]) continue;
+#pragma unroll
+      for (int k = 0; k < E; ++k) e[i][k] *= inv;
+      st_vec<T>(Y + r * L + col[i], e[i]);
+    }
+  };
+  int64_t r = blockIdx.x;
+  u32x4_t xa[NV], xb[NV];
+  load_row(r, xa);
+  for (; r < rows; r += 2 * step) {
+    load_row(r + step, xb);
+    do_row(r, xa);
+    if (r + step >= rows) break;
+    load_row(r + 2 * step, xa);
+    do_row(r + step, xb);
+  }
+}
+
+// Persistent row waves: eight per CU (LayerNorm; softmax takes twice as many).
 static int ln_waves() {
   int dev = 0, n = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
@@ -245,6 +322,17 @@ hipError_t launch_row_wave_t(const RowArgs& a, hipStream_t st) {
   constexpr int E = kEpv<T>;
   const int64_t nv = (a.len + 64 * E - 1) / (64 * E);
   const dim3 grid((unsigned)a.rows), block(64);
+  if (a.op == MK_OP_SOFTMAX) {
+    // (sixteen waves per CU: fewer registers than the LayerNorm waves)
+    const dim3 pg((unsigned)std::min<int64_t>(a.rows, 2 * ln_waves()));
+    switch (nv) {
+      case 1: hipLaunchKernelGGL((softmax_rows_kernel<T, 1>), pg, block, 0, st, a); break;
+      case 2: hipLaunchKernelGGL((softmax_rows_kernel<T, 2>), pg, block, 0, st, a); break;
+      case 3: case 4: hipLaunchKernelGGL((softmax_rows_kernel<T, 4>), pg, block, 0, st, a); break;
+      default: hipLaunchKernelGGL((softmax_rows_kernel<T, 8>), pg, block, 0, st, a); break;
+    }
+    return hipGetLastError();
+  }
   if (a.op == MK_OP_LAYERNORM) {
     const dim3 pg((unsigned)std::min<int64_t>(a.rows, ln_waves()));
     switch (nv) {
