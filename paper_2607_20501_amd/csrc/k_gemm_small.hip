@@ -131,9 +131,39 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(GemmArgs a) {
   if (a.terminal == TERM_NONE) return;
   // Per-row partials over this wave's 32 columns (lanes of one half), then
   // over the two waves of the tile's 64 columns.
+  if (a.terminal == TERM_ROWSUM) {
+    // All 16 rows at once by a halving butterfly over the 32 lanes lr: at
+    // the step across lane bit b a lane keeps the half of its values
+    // selected by that bit and adds the partner's copy of it; after bits
+    // 4..1 lane lr holds row r = lr / 2, and a last exchange across bit 0
+    // completes it (16 exchanges instead of 5 per row).
+    float x[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) x[r] = col_ok ? v[r] : 0.f;
+#define MK_SMALL_STEP(O, H)                                                         \
+  {                                                                                 \
+    const bool up = (lr & (O)) != 0;                                                \
+    _Pragma("unroll") for (int k = 0; k < (H); ++k) {                               \
+      const float keep = up ? x[k + (H)] : x[k];                                    \
+      const float send = up ? x[k] : x[k + (H)];                                    \
+      x[k] = keep + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(send), \
+                                                               ((O) << 10) | 0x1F));  \
+    }                                                                               \
+  }
+    MK_SMALL_STEP(16, 8)
+    MK_SMALL_STEP(8, 4)
+    MK_SMALL_STEP(4, 2)
+    MK_SMALL_STEP(2, 1)
+#undef MK_SMALL_STEP
+    x[0] += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x[0]), (1 << 10) | 0x1F));
+    if ((lr & 1) == 0) {
+      const int r = lr >> 1;
+      red[wn][wm * 32 + (r >> 2) * 8 + lh * 4 + (r & 3)][1] = x[0];
+    }
+  }
   const float cnt = (float)min<int64_t>(32, max<int64_t>(0, a.N - n0));
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
+  for (int r = 0; r < 16 && a.terminal != TERM_ROWSUM; ++r) {
     const int trow = wm * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
     float p0, p1;
     if (a.terminal == TERM_LAYERNORM) {
