@@ -124,6 +124,21 @@ __device__ __forceinline__ TileCoord tile_of(int bid, int tiles_m, int tiles_n) 
   return {first_m + r % gsize, r / gsize};
 }
 
+// Work item of a persistent walk: a tile, or one row sub-tile of a tile.
+struct Item {
+  TileCoord tc;
+  int sub;   // row sub-tile, -1 for the whole tile
+};
+
+// Tail split of a persistent walk over `tiles` tiles by G workgroups: the
+// tiles past the last whole round (all of them when tiles < G) are cut along
+// M into 8 (or 4) row sub-tiles when that many of each fit in one round, so
+// the last round takes a fraction of a tile's time.  1: no split.
+__host__ __device__ inline int tail_split(int tiles, int G) {
+  const int rem = tiles % G;
+  return rem == 0 ? 1 : rem * 8 <= G ? 8 : rem * 4 <= G ? 4 : 1;
+}
+
 // Global operand access through buffer resources: a lane whose element lies
 // outside the operand gets an offset beyond the descriptor's range and reads
 // zeros, so ragged M / N / K tails need no branches.
@@ -255,6 +270,19 @@ __device__ __forceinline__ void mfma_step(const Frags<NJ, T>& f, f32x16 (&acc)[4
     }
 }
 
+// One 32 x 32 tile update from a sub-step's fragment pair (as in mfma_step).
+template <typename T>
+__device__ __forceinline__ f32x16 mfma1(const typename MfmaType<T>::frag& x,
+                                        const typename MfmaType<T>::frag& y, f32x16 c) {
+  if constexpr (sizeof(T) == 2) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, c, 0, 0, 0);
+  } else {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) c = __builtin_amdgcn_mfma_f32_32x32x2f32(x[t], y[t], c, 0, 0, 0);
+    return c;
+  }
+}
+
 // vmcnt(n) with the other counters left alone (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vm() {
@@ -373,7 +401,7 @@ template <typename T, int NJ, bool kBiasReluSum>
 __device__ __forceinline__ void gap_from_acc(const GemmArgs& a, const f32x16 (&acc)[4][NJ],
                                              int64_t m0, int64_t n0, int rowbase, int colbase,
                                              int wn, int lr, int lh, int pre,
-                                             const float* rbias, float* red) {
+                                             const float* rbias, float* red, int ni = 4) {
   const int kind = a.pool;
   const float pp = a.pool_p, idv = pool_id(kind);
   const int64_t PQ = a.cv_P * a.cv_Q;
@@ -382,7 +410,7 @@ __device__ __forceinline__ void gap_from_acc(const GemmArgs& a, const f32x16 (&a
   const int c_end = (int)min<int64_t>(a.N - n0, 1 << 30);
   const int c_bnd = (int)min<int64_t>((img0 + 1) * PQ - n0, 1 << 30);
 #pragma unroll 1
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < ni; ++i) {
     const int64_t rb = m0 + rowbase + i * 32;
     const int mrem = (int)min<int64_t>(a.M - rb, 1 << 30);
     float bc[16];
@@ -468,9 +496,11 @@ __device__ __forceinline__ void gap_from_acc(const GemmArgs& a, const f32x16 (&a
 // slice never crosses an (r, s) boundary since C is a multiple of its depth).
 template <typename T>
 __device__ __forceinline__ uint32_t conv_koff(const GemmArgs& a, int64_t k0) {
-  const int64_t rs = k0 / a.cv_C, c0 = k0 % a.cv_C;
-  const int64_t r = rs / a.cv_S, s = rs % a.cv_S;
-  return (uint32_t)(((r * a.cv_Wp + s) * a.cv_C + c0) * (int64_t)sizeof(T));
+  // 32-bit: K = C*R*S and the window's extent in the padded input fit.
+  const uint32_t k = (uint32_t)k0, C = (uint32_t)a.cv_C, S = (uint32_t)a.cv_S;
+  const uint32_t rs = k / C, c0 = k - rs * C;
+  const uint32_t r = rs / S, s = rs - r * S;
+  return ((r * (uint32_t)a.cv_Wp + s) * C + c0) * (uint32_t)sizeof(T);
 }
 
 // LDS bytes of the epilogue: per wave a 32-row slab (8 row groups of kSlabU
@@ -527,6 +557,27 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   float* rbias = (float*)(smem + (PIPE ? kEpiOff : kSmemMain));
   const int tiles_m = (int)((a.M + BM - 1) / BM), tiles_n = (int)((a.N + BN - 1) / BN);
   const int tiles = tiles_m * tiles_n;
+  // Work items: whole tiles, then (pipelined conv) the row sub-tiles of SR
+  // rows of the tiles left after the last whole round.
+  const int G = (int)gridDim.x;
+  const int tsplit = (CONV && PIPE) ? tail_split(tiles, G) : 1;
+  const int tfirst = tsplit > 1 ? tiles - tiles % G : tiles;
+  const int trem = tiles - tfirst;
+  const int items = tfirst + trem * tsplit;
+  const int SR = BM / tsplit;
+  auto item_of = [&](int u) -> Item {
+    if (u < tfirst) return {tile_of(u, tiles_m, tiles_n), -1};
+    const int k = u - tfirst;
+    return {tile_of(tfirst + k % trem, tiles_m, tiles_n), k / trem};
+  };
+  auto row0_of = [&](const Item& it) -> int64_t {
+    return (int64_t)it.tc.tm * BM + (it.sub < 0 ? 0 : it.sub * SR);
+  };
+  // This workgroup's next item from u on (sub-tiles starting past M skipped).
+  auto next_item = [&](int u) {
+    while (u < items && u >= tfirst && row0_of(item_of(u)) >= a.M) u += G;
+    return u;
+  };
   const int64_t z = blockIdx.y, bb = z / a.heads, hh = z % a.heads;
   const T* A = (const T*)a.A + a.a_off + bb * a.a_sb + hh * a.a_sh;
   const T* B = (const T*)a.B + a.b_off + bb * a.b_sb + hh * a.b_sh;
@@ -540,9 +591,9 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
 
   SliceLoader<WAVES, BM, T, RB> la;
   SliceLoader<WAVES, BN, T, RB> lb;
-  auto init_loaders = [&](const TileCoord& t) {
-    const int64_t m0 = (int64_t)t.tm * BM, n0 = (int64_t)t.tn * BN;
-    la.init(A, a.M, a.lda, m0);
+  auto init_loaders = [&](const Item& it) {
+    const int64_t m0 = row0_of(it), n0 = (int64_t)it.tc.tn * BN;
+    la.init(A, it.sub < 0 ? a.M : min<int64_t>(a.M, m0 + SR), a.lda, m0);
     if (CONV) {
       const int64_t bytes = a.cv_Hp * a.cv_Wp * a.cv_C * (int64_t)sizeof(T) * (a.N / PQ);
       lb.init_gather(B, bytes, a.N, n0, [&](int64_t m) {
@@ -578,10 +629,25 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     else
       lb.issue(b_slot(ks), k0, a.K);
   };
+  // Sub-tile stages: A (its first 64 rows: one load per thread) in four 8 KB
+  // slots at 0, B in four 32 KB slots from 32 KB, so stage 0 sits where a
+  // whole tile's does (clear of the epilogue's LDS).
+  auto a_slot_s = [&](int ks) -> char* { return smem + (ks & 3) * 8192; };
+  auto b_slot_s = [&](int ks) -> char* { return smem + 32768 + (ks & 3) * 32768; };
+  auto issue_sub = [&](int ks) {
+    const int64_t k0 = (int64_t)ks * BK;
+    la.template issue_part<0, 1>(a_slot_s(ks), k0, a.K);
+    if (CONV)
+      lb.issue(b_slot_s(ks), k0, a.K, conv_koff<T>(a, k0));
+    else
+      lb.issue(b_slot_s(ks), k0, a.K);
+  };
 
-  int v = blockIdx.x;
-  TileCoord tc = tile_of(v, tiles_m, tiles_n);
-  init_loaders(tc);
+  int v = next_item((int)blockIdx.x);
+  if (v >= items) return;
+  Item it = item_of(v);
+  TileCoord tc = it.tc;
+  init_loaders(it);
   if (!PIPE) {
 #pragma unroll
     for (int s = 0; s < kStages - 1; ++s)
@@ -640,19 +706,21 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   // Pipelined conv: this thread's channel-bias value of the tile (rows
   // threadIdx.x < BM), loaded with the tile's first stages and written to LDS
   // once the main loop has released it.
-  auto load_bias_reg = [&](const TileCoord& t) -> float {
+  auto load_bias_reg = [&](const Item& t) -> float {
     if (!(CONV && PIPE) || pre_ch < 0 || (int)threadIdx.x >= BM) return 0.f;
-    const int64_t r = (int64_t)t.tm * BM + threadIdx.x;
+    const int64_t r = row0_of(t) + threadIdx.x;
     return r < a.M ? ld<T>((const T*)a.epi.ptr[pre_ch], r) : 0.f;
   };
-  float bias_reg = load_bias_reg(tc);
+  float bias_reg = load_bias_reg(it);
   bool staged0 = false;   // this tile's stage 0 was issued during the last epilogue
   constexpr int kEpiVmem = (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
                             SIG == kSigBiasGeluTanhScale)
                                ? 16
                                : 0;
   for (;;) {
-    const int64_t m0 = (int64_t)tc.tm * BM, n0 = (int64_t)tc.tn * BN;
+    const int64_t m0 = row0_of(it), n0 = (int64_t)tc.tn * BN;
+    const bool subt = CONV && PIPE && it.sub >= 0;
+    const int rows_it = subt ? SR : BM;
     f32x16 acc[4][NJ];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -661,7 +729,39 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    if (PIPE) {
+    if (PIPE && subt) {
+      // Row sub-tile: waves wm with wm*32 < SR compute rows wm*32 .. +31 of
+      // it into acc[0]; every wave loads.  Three stages in flight; one
+      // barrier per stage (it also orders the refill of the slot read in the
+      // previous stage after every wave's reads of it).
+      const bool cw = wm * 32 < SR;
+      if (!staged0) issue_sub(0);
+      issue_sub(1);
+      issue_sub(2);
+      for (int ks = 0; ks < nk; ++ks) {
+        wait_vm<2 * (1 + LB)>();
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        issue_sub(ks + 3);
+        if (cw) {
+          typedef typename MfmaType<T>::frag F;
+          const char* ca = a_slot_s(ks);
+          const char* cb = b_slot_s(ks);
+#pragma unroll
+          for (int kk = 0; kk < KSUB; ++kk) {
+            F fb[NJ];
+            const F fa = *(const F*)(ca + lds_off<RB>(wm * 32 + lr, kk * 2 + lh));
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+              fb[j] = *(const F*)(cb + lds_off<RB>(colbase + j * 32 + lr, kk * 2 + lh));
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) acc[0][j] = mfma1<T>(fa, fb[j], acc[0][j]);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else if (PIPE) {
       // Stages 0 and 1 go now.  Stage s: sub-steps 0..3,
       // fragments one sub-step ahead of the MFMAs that use them; A(s+2) is
       // issued over sub-steps 0 and 1 (its slot held stage s-1, released by
@@ -773,20 +873,26 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     wait_vm<0>();
     __syncthreads();
     if (CONV && PIPE && pre_ch >= 0) {
-      if ((int)threadIdx.x < BM) rbias[threadIdx.x] = bias_reg;
+      int tb = (int)threadIdx.x;   // opaque copy: the address is not kept live
+      asm volatile("" : "+v"(tb));
+      if (tb < BM) rbias[tb] = bias_reg;
       __syncthreads();
     }
-    const int vn = v + (int)gridDim.x;
-    const bool more = kPersist && vn < tiles;
+    const int vn = next_item(v + G);
+    const bool more = kPersist && vn < items;
     // The next tile's stage 0 loads while this epilogue runs (its LDS is
     // clear of slots A0 and B0; every read of the last stages is done).
-    TileCoord tc_next = tc;
+    Item it_next = it;
     if (PIPE && more) {
-      tc_next = tile_of(vn, tiles_m, tiles_n);
-      init_loaders(tc_next);
-      issue_a(0);
-      issue_b(0);
-      bias_reg = load_bias_reg(tc_next);
+      it_next = item_of(vn);
+      init_loaders(it_next);
+      if (CONV && it_next.sub >= 0) {
+        issue_sub(0);
+      } else {
+        issue_a(0);
+        issue_b(0);
+      }
+      bias_reg = load_bias_reg(it_next);
     }
     staged0 = PIPE && more;
     // Lane-derived values of the epilogue, recomputed here from an opaque
@@ -799,7 +905,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     const int lane_e = tid_e & 63, w_e = tid_e >> 6;
     const int wn_e = w_e % WN;
     const int lr = lane_e & 31, lh = lane_e >> 5;
-    const int rowbase = (w_e / WN) * 128, colbase = wn_e * WTN;
+    const int rowbase = (w_e / WN) * (subt ? 32 : 128), colbase = wn_e * WTN;
     // Epilogue lane roles: 8-column group q and row group rg of the slab;
     // the 8 lanes of a row (same rg) are lanes rg, rg+8, ..., rg+56.
     const int q = lane_e >> 3, rg = lane_e & 7;
@@ -1032,7 +1138,9 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       }
     };
     if (SIG == kSigConvBiasReluGap || (CONV && term == TERM_GAP)) {
-      gap_from_acc<T, NJ, SIG == kSigConvBiasReluGap>(a, acc, m0, n0, rowbase, colbase, wn, lr, lh, pre_ch, rbias, red);
+      gap_from_acc<T, NJ, SIG == kSigConvBiasReluGap>(a, acc, m0, n0, rowbase, colbase, wn, lr, lh,
+                                                       pre_ch, rbias, red,
+                                                       subt ? (rowbase < SR ? 1 : 0) : 4);
     } else if constexpr (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
                          SIG == kSigBiasGeluTanhScale) {
       // (The softmax-partial chain keeps the rolled loop: unrolled, its
@@ -1062,7 +1170,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     }
     if (term != TERM_NONE) {
       __syncthreads();
-      for (int lrow = threadIdx.x; lrow < BM; lrow += THREADS) {
+      for (int lrow = threadIdx.x; lrow < rows_it; lrow += THREADS) {
         const int64_t row = m0 + lrow;
         if (row >= a.M) break;
         if (CONV) {   // GAP partials of this position tile, per image slot
@@ -1117,7 +1225,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_s_barrier();
     v = vn;
-    tc = tc_next;
+    it = it_next;
+    tc = it.tc;
   }
 }
 
@@ -1321,11 +1430,15 @@ hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
   const int64_t bn = gemm_mfma_tile_n(dtype, a);
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + bn - 1) / bn);
   // The 256 x 256 kernels run persistent workgroups, one per CU across the
-  // batch; the ring conv kernel one workgroup per tile.
+  // batch; the ring conv kernel one workgroup per tile.  Conv: fewer tiles
+  // than CUs are all cut into row sub-tiles (as the kernel's tail split
+  // does for the last round), one workgroup each.
   int64_t gx = tiles;
   if (bn == 256) {
     const int64_t z = (int64_t)a.batch * a.heads;
-    gx = std::min<int64_t>(tiles, std::max<int64_t>(1, (cu_count() + z - 1) / z));
+    const int64_t g = std::max<int64_t>(1, (cu_count() + z - 1) / z);
+    gx = std::min<int64_t>(tiles, g);
+    if (a.conv && tiles < g) gx = tiles * tail_split((int)tiles, (int)g);
   }
   dim3 grid((unsigned)gx, (unsigned)(a.batch * a.heads));
   if (dtype == MK_BF16)

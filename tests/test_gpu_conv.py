@@ -47,6 +47,17 @@ POOL_CASES = [dict(N=3, C=32, H=20, W=20, K=40), dict(N=2, C=64, H=16, W=16, K=3
               dict(N=2, C=8, H=9, W=7, K=5)]
 
 
+def test_conv_tail_split():
+    # 294 position tiles of 256 on the persistent kernel: the 38 tiles past
+    # the last whole round of 256 workgroups run as 64-row sub-tiles, and
+    # K=40 leaves the second row-wave of each sub-tile 8 rows
+    shape = dict(N=24, C=64, H=56, W=56, K=40)
+    print(f"conv tail split {shape}", flush=True)
+    module = workloads.conv_relu_gap(dtype="bf16", **shape)
+    rep, m, *_ = run_parity(module, "fused")
+    assert rep["pass"], describe(rep)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("pool,p", [("GMP", 2.0), ("LPPOOL", 2.0), ("LPPOOL", 3.0)])
 @pytest.mark.parametrize("shape", POOL_CASES)
