@@ -254,18 +254,22 @@ __device__ __forceinline__ void load_frags(const char* la, const char* lb, int k
 // instruction's k = 8*lh .. 8*lh+7).  fp32: the lane's 4 k values feed four
 // 32x32x2 MFMAs, instruction t taking k = 4*lh + t of the chunk pair; A and B
 // use the same assignment, so the sum over k is unchanged.
-template <int NJ, typename T>
+// TR: operands swapped, so tile (i, j) accumulates the transpose (a lane
+// holds one row of A's tile i and 16 of B's tile j).
+template <int NJ, typename T, bool TR = false>
 __device__ __forceinline__ void mfma_step(const Frags<NJ, T>& f, f32x16 (&acc)[4][NJ]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
+      const auto& x = TR ? f.b[j] : f.a[i];
+      const auto& y = TR ? f.a[i] : f.b[j];
       if constexpr (sizeof(T) == 2) {
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, acc[i][j], 0, 0, 0);
       } else {
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.a[i][t], f.b[j][t], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(x[t], y[t], acc[i][j], 0, 0, 0);
       }
     }
 }
@@ -409,6 +413,44 @@ __device__ __forceinline__ void gap_from_acc(const GemmArgs& a, const f32x16 (&a
   // columns of this lane relative to the tile, against N and the image bound
   const int c_end = (int)min<int64_t>(a.N - n0, 1 << 30);
   const int c_bnd = (int)min<int64_t>((img0 + 1) * PQ - n0, 1 << 30);
+  if constexpr (kBiasReluSum) {
+    // Transposed tiles: lane lr of tile (i, j) holds channel rowbase+i*32+lr
+    // at the 16 positions j*32 + (r/4)*8 + lh*4 + r%4 of the wave's columns,
+    // so each sum is lane-local; the two lane halves then combine.  Waves
+    // whose columns are all in range and in one image take the plain sum.
+    const float alpha = a.alpha;
+    const bool plain = colbase + NJ * 32 <= c_end && colbase + NJ * 32 <= c_bnd;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (i >= ni) break;
+      const int lrow = rowbase + i * 32 + lr;
+      const float b = pre >= 0 ? rbias[lrow] : 0.f;
+      float x0 = 0.f, x1 = 0.f;
+      if (plain) {
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) x0 += fmaxf(fmaf(acc[i][j][r], alpha, b), 0.f);
+      } else {
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int p = colbase + j * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+            const float c = p < c_end ? fmaxf(fmaf(acc[i][j][r], alpha, b), 0.f) : 0.f;
+            x0 += p < c_bnd ? c : 0.f;
+            x1 += p < c_bnd ? 0.f : c;
+          }
+      }
+      x0 += lane_xor<32>(x0);
+      x1 += lane_xor<32>(x1);
+      if (lh == 0) {
+        red[(wn * 256 + lrow) * 2] = x0;
+        red[(wn * 256 + lrow) * 2 + 1] = x1;
+      }
+    }
+    return;
+  }
 #pragma unroll 1
   for (int i = 0; i < ni; ++i) {
     const int64_t rb = m0 + rowbase + i * 32;
@@ -535,6 +577,9 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   constexpr int WTN = BN / WN;        // wave tile columns
   constexpr int NJ = WTN / 32;        // 32-wide column tiles per wave
   constexpr bool kPersist = PIPE != 0;
+  // Conv bias+ReLU+GAP: transposed accumulators (a lane holds one channel),
+  // so the pooling sums are lane-local.
+  constexpr bool kTr = SIG == kSigConvBiasReluGap;
   static_assert(PIPE == 0 || (KSUB == 4 && kABytes == 32768 && kBBytes == 32768),
                 "the pipelined loop is k64 stages of a 256 x 256 tile");
   // Pipelined slots: A0 0, B0 32K, A1 64K, A2 96K, B1 128K; the epilogue
@@ -756,7 +801,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
             for (int j = 0; j < NJ; ++j)
               fb[j] = *(const F*)(cb + lds_off<RB>(colbase + j * 32 + lr, kk * 2 + lh));
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) acc[0][j] = mfma1<T>(fa, fb[j], acc[0][j]);
+            for (int j = 0; j < NJ; ++j)
+              acc[0][j] = kTr ? mfma1<T>(fb[j], fa, acc[0][j]) : mfma1<T>(fa, fb[j], acc[0][j]);
           }
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -801,7 +847,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
             la.template issue_part<0, kA0>(a_slot(ks + 2), (int64_t)(ks + 2) * BK, a.K);
           if constexpr (sub == 1)
             la.template issue_part<kA0, LA>(a_slot(ks + 2), (int64_t)(ks + 2) * BK, a.K);
-          mfma_step<NJ, T>(use, acc);
+          mfma_step<NJ, T, kTr>(use, acc);
 #pragma unroll
           for (int g = 0; g < kReadPairs; ++g) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
@@ -826,7 +872,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         __builtin_amdgcn_sched_barrier(0);
         load_frags<NJ, T, RB>(a_slot(ks + 1), b_slot(ks + 1), 0, rowbase, colbase, lr, lh, f0);
         issue_b(ks + 2);
-        mfma_step<NJ, T>(f1, acc);
+        mfma_step<NJ, T, kTr>(f1, acc);
 #pragma unroll
         for (int g = 0; g < kReadPairs; ++g) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
@@ -862,7 +908,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int sub = 0; sub < KSUB; ++sub) {
-          mfma_step<NJ, T>(f[sub], acc);
+          mfma_step<NJ, T, kTr>(f[sub], acc);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
