@@ -27,13 +27,23 @@ struct KrscArgs {
 // image of the input-packing grid (one launch packs both operands): workgroup
 // b of nb takes elements b*256*8 + t, stepping by 256, for 8 steps, and the
 // rest in grid-stride order.
+// Eight elements per pass: all eight loads are issued before the stores.
 template <typename T>
-__device__ __forceinline__ void pack_krsc_part(const T* w, T* wp, int64_t K, int64_t C, int64_t R,
-                                               int64_t S, int64_t b, int64_t nb) {
-  const int64_t total = K * R * S * C;
-  for (int64_t i = b * 256 + threadIdx.x; i < total; i += nb * 256) {
-    const int64_t c = i % C, s = (i / C) % S, r = (i / (C * S)) % R, k = i / (C * S * R);
-    wp[i] = w[((k * C + c) * R + r) * S + s];
+__device__ __forceinline__ void pack_krsc_part(const T* __restrict__ w, T* __restrict__ wp,
+                                               int64_t K, int64_t C, int64_t R, int64_t S,
+                                               int64_t b, int64_t nb) {
+  const int64_t total = K * R * S * C, step = nb * 256;
+  for (int64_t i0 = b * 256 + threadIdx.x; i0 < total; i0 += 8 * step) {
+    T v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t i = i0 + u * step;
+      const int64_t c = i % C, s = (i / C) % S, r = (i / (C * S)) % R, k = i / (C * S * R);
+      v[u] = i < total ? w[((k * C + c) * R + r) * S + s] : T(0);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (i0 + u * step < total) wp[i0 + u * step] = v[u];
   }
 }
 
@@ -84,6 +94,72 @@ __global__ __launch_bounds__(256) void pack_nhwc_rows_kernel(const T* x, T* xp, 
     uint4 v = make_uint4(0, 0, 0, 0);
     if (inside && w >= 0 && w < W) v = *(const uint4*)&tile[w][cc * E];
     *(uint4*)(dst + wp * C + cc * E) = v;
+  }
+}
+
+// Block form (C and W multiples of the 16-byte chunk E): no LDS.  Thread g
+// takes an E x E block (E channels at E consecutive positions of one input
+// row): E 16-byte loads, one per channel row, transposed in registers into E
+// 16-byte stores, one per position.  Channel blocks vary fastest across
+// threads, so a wave's stores cover whole positions (all C channels
+// contiguous).  Threads past the blocks write the zero border (one 16-byte
+// chunk each).  The weights are packed by the first workgroups, which start
+// first (their element-wise gathers are latency-bound).
+template <typename T>
+__global__ __launch_bounds__(256) void pack_nhwc_blocks_kernel(const T* x, T* xp, int N, int C,
+                                                               int H, int W, int pad,
+                                                               int64_t n_blk, int64_t n_zero,
+                                                               int wg_data, KrscArgs<T> kw) {
+  constexpr int E = 16 / (int)sizeof(T);
+  const int wg_w = (int)gridDim.x - wg_data;   // weight workgroups come first
+  if ((int)blockIdx.x < wg_w) {
+    pack_krsc_part(kw.w, kw.wp, kw.K, C, kw.R, kw.S, (int64_t)blockIdx.x, (int64_t)wg_w);
+    return;
+  }
+  const int CB = C / E, PB = W / E;
+  const int64_t Hp = H + 2 * pad, Wp = W + 2 * pad;
+  const int64_t g = (int64_t)(blockIdx.x - wg_w) * 256 + threadIdx.x;
+  if (g < n_blk) {
+    int64_t t = g;
+    const int cb = (int)(t % CB);
+    t /= CB;
+    const int pb = (int)(t % PB);
+    t /= PB;
+    const int h = (int)(t % H);
+    const int64_t n = t / H;
+    const T* src = x + ((n * C + (int64_t)cb * E) * H + h) * W + (int64_t)pb * E;
+    union Chunk {
+      uint4 u;
+      T e[E];
+    } v[E], o;
+#pragma unroll
+    for (int k = 0; k < E; ++k) v[k].u = *(const uint4*)(src + (int64_t)k * H * W);
+    T* dst = xp + ((n * Hp + h + pad) * Wp + (int64_t)pb * E + pad) * C + (int64_t)cb * E;
+#pragma unroll
+    for (int q = 0; q < E; ++q) {
+#pragma unroll
+      for (int k = 0; k < E; ++k) o.e[k] = v[k].e[q];
+      *(uint4*)(dst + (int64_t)q * C) = o.u;
+    }
+  } else if (g < n_blk + n_zero) {
+    // border chunk: the 2*pad padded rows, then the 2*pad side positions of
+    // each interior row, per image
+    const int64_t rows_part = 2 * pad * Wp * CB;
+    const int64_t per_img = rows_part + (int64_t)H * 2 * pad * CB;
+    const int64_t z = g - n_blk, n = z / per_img;
+    int64_t r = z % per_img, hp, wp;
+    const int cb = (int)(r % CB);
+    if (r < rows_part) {
+      const int64_t row = r / (Wp * CB);
+      hp = row < pad ? row : H + row;
+      wp = (r / CB) % Wp;
+    } else {
+      r -= rows_part;
+      const int64_t sd = (r / CB) % (2 * pad);
+      hp = r / (2 * pad * CB) + pad;
+      wp = sd < pad ? sd : W + sd;
+    }
+    *(uint4*)(xp + ((n * Hp + hp) * Wp + wp) * C + (int64_t)cb * E) = make_uint4(0, 0, 0, 0);
   }
 }
 
@@ -189,7 +265,16 @@ static void launch_pack_t(const ConvArgs& a, void* xp, void* wp, hipStream_t st)
   const int64_t Hp = a.H + 2 * a.pad, HWp = Hp * (a.W + 2 * a.pad);
   const unsigned cb = (unsigned)((a.C + 63) / 64);
   const KrscArgs<T> kw{(const T*)a.w, (T*)wp, a.K, a.R, a.S};
-  if (a.W <= 64 && a.W % E == 0 && (uintptr_t)a.x % 16 == 0) {
+  if (a.C % E == 0 && a.W % E == 0 && (uintptr_t)a.x % 16 == 0) {
+    const int64_t n_blk = a.N * a.H * (a.W / E) * (a.C / E);
+    const int64_t Wp = a.W + 2 * a.pad;
+    const int64_t n_zero = a.N * (2 * a.pad * Wp + a.H * 2 * a.pad) * (a.C / E);
+    const int64_t wg_data = (n_blk + n_zero + 255) / 256;
+    const unsigned wg_w = krsc_slices(a, 1);
+    hipLaunchKernelGGL(pack_nhwc_blocks_kernel<T>, dim3((unsigned)(wg_data + wg_w)), dim3(256), 0,
+                       st, (const T*)a.x, (T*)xp, (int)a.N, (int)a.C, (int)a.H, (int)a.W,
+                       (int)a.pad, n_blk, n_zero, (int)wg_data, kw);
+  } else if (a.W <= 64 && a.W % E == 0 && (uintptr_t)a.x % 16 == 0) {
     const unsigned z = (unsigned)a.N + krsc_slices(a, Hp * cb);
     hipLaunchKernelGGL(pack_nhwc_rows_kernel<T>, dim3((unsigned)Hp, cb, z), dim3(256), 0, st,
                        (const T*)a.x, (T*)xp, a.N, a.C, a.H, a.W, a.pad, kw);
