@@ -1276,38 +1276,33 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   }
 }
 
-// B(k, n) of a [K, N] operand (batched) -> dst[z][n][k], K contiguous.  One
-// 64 x 64 tile per workgroup through LDS; 16-byte global accesses on both
-// sides (K and N are multiples of the 16-byte chunk).
+// B(k, n) of a [K, N] operand (batched) -> dst[z][n][k], K contiguous (K and
+// N are multiples of the 16-byte chunk of E elements).  No LDS: a lane moves
+// one E x E block, E 16-byte loads along n transposed in registers into E
+// 16-byte stores along k.  Lane (kb, nb) = (lane % 8, lane / 8) of wave w
+// takes k-block 8*blockIdx.y + kb and n-block 8*(4*blockIdx.x + w) + nb, so
+// every load and every store instruction covers eight 128-byte runs.
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_b_kernel(GemmArgs a, T* dst) {
   constexpr int E = 16 / (int)sizeof(T);    // elements per chunk
-  constexpr int CPR = 64 / E;               // chunks per 64-element tile row
-  constexpr int RPP = 256 / CPR;            // tile rows per pass
-  __shared__ __attribute__((aligned(16))) T tile[64][64 + E];
   const int64_t z = blockIdx.z, bb = z / a.heads, hh = z % a.heads;
   const T* src = (const T*)a.B + a.b_off + bb * a.b_sb + hh * a.b_sh;
-  const int64_t k0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
-  const int t = threadIdx.x, r = t / CPR, ce = (t % CPR) * E;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t k0 = ((int64_t)blockIdx.y * 8 + (lane & 7)) * E;
+  const int64_t n0 = (((int64_t)blockIdx.x * 4 + w) * 8 + (lane >> 3)) * E;
+  if (k0 >= a.K || n0 >= a.N) return;
+  union Chunk {
+    uint4 u;
+    T e[E];
+  } v[E], o;
 #pragma unroll
-  for (int h = 0; h < 64 / RPP; ++h) {
-    const int64_t k = k0 + r + h * RPP, n = n0 + ce;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (k < a.K && n < a.N) v = *(const uint4*)(src + k * a.ldb + n);
-    *(uint4*)&tile[r + h * RPP][ce] = v;
-  }
-  __syncthreads();
-  T* out = dst + z * a.N * a.K;
+  for (int u = 0; u < E; ++u) v[u].u = *(const uint4*)(src + (k0 + u) * a.ldb + n0);
+  T* out = dst + z * a.N * a.K + n0 * a.K + k0;
 #pragma unroll
-  for (int h = 0; h < 64 / RPP; ++h) {
-    const int nl = r + h * RPP;
-    const int64_t n = n0 + nl, k = k0 + ce;
-    if (n < a.N && k < a.K) {
-      T v[E];
+  for (int q = 0; q < E; ++q) {
 #pragma unroll
-      for (int e = 0; e < E; ++e) v[e] = tile[ce + e][nl];
-      *(uint4*)(out + n * a.K + k) = __builtin_bit_cast(uint4, v);
-    }
+    for (int u = 0; u < E; ++u) o.e[u] = v[u].e[q];
+    *(uint4*)(out + q * a.K) = o.u;
   }
 }
 
@@ -1337,7 +1332,8 @@ int64_t gemm_mfma_bt_bytes(int dtype, const GemmArgs& a) {
 }
 
 hipError_t launch_transpose_b(int dtype, const GemmArgs& a, void* dst, hipStream_t st) {
-  dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)((a.K + 63) / 64),
+  const int64_t E = dtype == MK_BF16 ? 8 : 4;
+  dim3 grid((unsigned)((a.N + 32 * E - 1) / (32 * E)), (unsigned)((a.K + 8 * E - 1) / (8 * E)),
             (unsigned)(a.batch * a.heads));
   if (dtype == MK_BF16)
     hipLaunchKernelGGL(transpose_b_kernel<bf16>, grid, dim3(256), 0, st, a, (bf16*)dst);
