@@ -995,7 +995,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
                                  : cbase + row * a.ldc + col0;
       if constexpr (SIG == kSigGeluErf) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = gelu_erf(v[e]);
+        for (int e = 0; e < 8; ++e) v[e] = sizeof(T) == 2 ? gelu_erf_bf16out(v[e]) : gelu_erf(v[e]);
       } else if constexpr (SIG == kSigAdd) {
         float t8[8];
         if (valid == 8 && vec_ok) {
