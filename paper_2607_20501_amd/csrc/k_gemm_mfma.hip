@@ -640,12 +640,16 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     const int64_t m0 = row0_of(it), n0 = (int64_t)it.tc.tn * BN;
     la.init(A, it.sub < 0 ? a.M : min<int64_t>(a.M, m0 + SR), a.lda, m0);
     if (CONV) {
-      const int64_t bytes = a.cv_Hp * a.cv_Wp * a.cv_C * (int64_t)sizeof(T) * (a.N / PQ);
+      const int64_t bytes = a.cv_Hp * a.cv_Wp * a.cv_C * (int64_t)sizeof(T) *
+                            ((uint32_t)a.N / (uint32_t)PQ);
+      // 32-bit: positions and byte offsets in the padded input stay below
+      // 2^31 (64-bit divisions here cost more than a stage of MFMAs).
+      const uint32_t PQu = (uint32_t)PQ, Qu = (uint32_t)a.cv_Q, st = (uint32_t)a.cv_stride;
+      const uint32_t Hpu = (uint32_t)a.cv_Hp, Wpu = (uint32_t)a.cv_Wp, Cu = (uint32_t)a.cv_C;
       lb.init_gather(B, bytes, a.N, n0, [&](int64_t m) {
-        const int64_t n = m / PQ, pq = m % PQ;
-        const int64_t p = pq / a.cv_Q, q = pq % a.cv_Q;
-        return ((n * a.cv_Hp + p * a.cv_stride) * a.cv_Wp + q * a.cv_stride) * a.cv_C *
-               (int64_t)sizeof(T);
+        const uint32_t mu = (uint32_t)m, n = mu / PQu, pq = mu - n * PQu;
+        const uint32_t p = pq / Qu, q = pq - p * Qu;
+        return ((n * Hpu + p * st) * Wpu + q * st) * Cu * (uint32_t)sizeof(T);
       });
     } else {
       lb.init(B, a.N, a.ldb, n0);
