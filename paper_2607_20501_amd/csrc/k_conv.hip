@@ -37,9 +37,12 @@ __device__ __forceinline__ void pack_krsc_part(const T* __restrict__ w, T* __res
     T v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
+      // 32-bit: the weight tensor has fewer than 2^31 elements
       const int64_t i = i0 + u * step;
-      const int64_t c = i % C, s = (i / C) % S, r = (i / (C * S)) % R, k = i / (C * S * R);
-      v[u] = i < total ? w[((k * C + c) * R + r) * S + s] : T(0);
+      const uint32_t iu = (uint32_t)i, Cu = (uint32_t)C, Su = (uint32_t)S, Ru = (uint32_t)R;
+      const uint32_t q1 = iu / Cu, c = iu - q1 * Cu, q2 = q1 / Su, s = q1 - q2 * Su;
+      const uint32_t k = q2 / Ru, r = q2 - k * Ru;
+      v[u] = i < total ? w[((k * Cu + c) * Ru + r) * Su + s] : T(0);
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u)
@@ -120,13 +123,14 @@ __global__ __launch_bounds__(256) void pack_nhwc_blocks_kernel(const T* x, T* xp
   const int64_t Hp = H + 2 * pad, Wp = W + 2 * pad;
   const int64_t g = (int64_t)(blockIdx.x - wg_w) * 256 + threadIdx.x;
   if (g < n_blk) {
-    int64_t t = g;
-    const int cb = (int)(t % CB);
-    t /= CB;
-    const int pb = (int)(t % PB);
-    t /= PB;
-    const int h = (int)(t % H);
-    const int64_t n = t / H;
+    // 32-bit index arithmetic: block and chunk counts stay below 2^31
+    uint32_t t = (uint32_t)g;
+    const int cb = (int)(t % (uint32_t)CB);
+    t /= (uint32_t)CB;
+    const int pb = (int)(t % (uint32_t)PB);
+    t /= (uint32_t)PB;
+    const int h = (int)(t % (uint32_t)H);
+    const int64_t n = t / (uint32_t)H;
     const T* src = x + ((n * C + (int64_t)cb * E) * H + h) * W + (int64_t)pb * E;
     union Chunk {
       uint4 u;
@@ -144,22 +148,23 @@ __global__ __launch_bounds__(256) void pack_nhwc_blocks_kernel(const T* x, T* xp
   } else if (g < n_blk + n_zero) {
     // border chunk: the 2*pad padded rows, then the 2*pad side positions of
     // each interior row, per image
-    const int64_t rows_part = 2 * pad * Wp * CB;
-    const int64_t per_img = rows_part + (int64_t)H * 2 * pad * CB;
-    const int64_t z = g - n_blk, n = z / per_img;
-    int64_t r = z % per_img, hp, wp;
-    const int cb = (int)(r % CB);
+    const uint32_t CBu = (uint32_t)CB, Wpu = (uint32_t)Wp, p2 = 2u * (uint32_t)pad;
+    const uint32_t rows_part = p2 * Wpu * CBu;
+    const uint32_t per_img = rows_part + (uint32_t)H * p2 * CBu;
+    const uint32_t z = (uint32_t)(g - n_blk), n = z / per_img;
+    uint32_t r = z - n * per_img, hp, wp;
+    const int cb = (int)(r % CBu);
     if (r < rows_part) {
-      const int64_t row = r / (Wp * CB);
-      hp = row < pad ? row : H + row;
-      wp = (r / CB) % Wp;
+      const uint32_t row = r / (Wpu * CBu);
+      hp = row < (uint32_t)pad ? row : (uint32_t)H + row;
+      wp = (r / CBu) % Wpu;
     } else {
       r -= rows_part;
-      const int64_t sd = (r / CB) % (2 * pad);
-      hp = r / (2 * pad * CB) + pad;
-      wp = sd < pad ? sd : W + sd;
+      const uint32_t sd = (r / CBu) % p2;
+      hp = r / (p2 * CBu) + (uint32_t)pad;
+      wp = sd < (uint32_t)pad ? sd : (uint32_t)W + sd;
     }
-    *(uint4*)(xp + ((n * Hp + hp) * Wp + wp) * C + (int64_t)cb * E) = make_uint4(0, 0, 0, 0);
+    *(uint4*)(xp + (((int64_t)n * Hp + hp) * Wp + wp) * C + (int64_t)cb * E) = make_uint4(0, 0, 0, 0);
   }
 }
 

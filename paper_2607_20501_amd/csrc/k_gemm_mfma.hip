@@ -971,7 +971,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     const int64_t col0 = n0 + colbase + q * 8;
     const int valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
     // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0).
-    const int64_t img = CONV ? col0 / PQ : 0;
+    const int64_t img = CONV ? (int64_t)((uint32_t)col0 / (uint32_t)PQ) : 0;   // positions < 2^31
 
     // Compiled TERM_NONE chains store through a buffer resource over C.
     constexpr bool kBufStore = SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
