@@ -47,11 +47,14 @@ POOL_CASES = [dict(N=3, C=32, H=20, W=20, K=40), dict(N=2, C=64, H=16, W=16, K=3
               dict(N=2, C=8, H=9, W=7, K=5)]
 
 
-def test_conv_tail_split():
-    # 294 position tiles of 256 on the persistent kernel: the 38 tiles past
-    # the last whole round of 256 workgroups run as 64-row sub-tiles, and
-    # K=40 leaves the second row-wave of each sub-tile 8 rows
-    shape = dict(N=24, C=64, H=56, W=56, K=40)
+# Persistent bf16 conv with a split last round.  294 position tiles of 256:
+# the 38 tiles past the last whole round of 256 workgroups run as 64-row
+# sub-tiles, K=40 leaving the second row-wave of each sub-tile 8 rows.  40
+# tiles (fewer than the CUs): all cut into 64-row sub-tiles, K=100 giving a
+# full first sub-tile, a ragged second one (36 rows) and two empty ones.
+@pytest.mark.parametrize("shape", [dict(N=24, C=64, H=56, W=56, K=40),
+                                   dict(N=10, C=64, H=32, W=32, K=100)])
+def test_conv_tail_split(shape):
     print(f"conv tail split {shape}", flush=True)
     module = workloads.conv_relu_gap(dtype="bf16", **shape)
     rep, m, *_ = run_parity(module, "fused")
