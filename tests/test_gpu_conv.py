@@ -52,8 +52,11 @@ POOL_CASES = [dict(N=3, C=32, H=20, W=20, K=40), dict(N=2, C=64, H=16, W=16, K=3
 # sub-tiles, K=40 leaving the second row-wave of each sub-tile 8 rows.  40
 # tiles (fewer than the CUs): all cut into 64-row sub-tiles, K=100 giving a
 # full first sub-tile, a ragged second one (36 rows) and two empty ones.
+# K=300: two tile rows (294 tiles, the second row 44 channels deep), so the
+# split round mixes full sub-tiles, a ragged one and empty ones.
 @pytest.mark.parametrize("shape", [dict(N=24, C=64, H=56, W=56, K=40),
-                                   dict(N=10, C=64, H=32, W=32, K=100)])
+                                   dict(N=10, C=64, H=32, W=32, K=100),
+                                   dict(N=12, C=64, H=56, W=56, K=300)])
 def test_conv_tail_split(shape):
     print(f"conv tail split {shape}", flush=True)
     module = workloads.conv_relu_gap(dtype="bf16", **shape)
