@@ -140,22 +140,38 @@ typedef struct {
   int32_t uses_mfma;              /* 1: the contraction runs on the matrix cores */
 } mk_subkernel_info_t;
 
-/* Fill group_of_op[n_ops] with a preset decomposition.  preset 0 = split (one
- * subkernel per op, except that a BIAS, BIAS_CHANNEL or ADD joins the GEMM or
- * CONV2D that produces its input, directly or through bias / add steps that
- * joined it); preset 1 = fused (from each op, the longest group a family
- * accepts).  Host only. */
+/* Fill group_of_op[n_ops] with a preset decomposition.  The groupings follow
+ * the fusion guidance of the decomposition prompt (App. I.1, "FUSION-FRIENDLY
+ * GROUPINGS" and "FUSION EXAMPLES"): a contraction keeps its bias, element-wise
+ * activations, scaling and residual add; a reduction that needs a whole row
+ * (softmax) is its own subproblem unless an online form exists (attention).
+ * preset 0 = split (one subkernel per op, except that a BIAS, BIAS_CHANNEL or
+ * ADD joins the GEMM or CONV2D that produces its input, directly or through
+ * bias / add steps that joined it); preset 1 = fused (from each op, the
+ * longest group a family accepts).  Host only.  MK_E_INVALID_ARG on a null
+ * argument or an unknown preset; shape errors as for mk_module_create. */
 mk_status mk_decomposition_preset(const mk_module_desc* desc, int32_t preset,
                                   int32_t* group_of_op);
 
 /* Validate the module (shape inference) and the grouping, match every group to
- * a family and lay out the workspace.  Host only: no device is touched.
+ * a family and lay out the workspace.  This is the programmatic check of a
+ * decomposition (Sec. 3, "LLMDecompose agent": subproblems with shapes, whose
+ * coverage and interfaces are checked before any kernel runs; App. I.1,
+ * "VERIFICATION CRITERIA").  Host only: no device is touched.
  * group_of_op[i] is op i's group; groups are numbered 0,1,.. in op order.
- * On success *out owns a new module (free with mk_module_destroy). */
+ * On success *out owns a new module (free with mk_module_destroy); on an
+ * error *out is NULL and the status says why (MK_E_SHAPE, MK_E_DTYPE,
+ * MK_E_DECOMP, MK_E_INVALID_ARG). */
 mk_status mk_module_create(const mk_module_desc* desc, const int32_t* group_of_op,
                            mk_module** out);
 void mk_module_destroy(mk_module* m);
 
+/* Introspection of the plan: the module's and each subkernel's shapes,
+ * workspace placement, algorithmic flops / bytes and launches, so that run
+ * time and speedups can be attributed to subkernels (Sec. 3,
+ * "AllocateLLMBudget" and "Swap" act per subkernel; Sec. 1 states speedups
+ * as traceable to specific subkernels).  Host only; MK_E_INVALID_ARG on a
+ * null argument or a subkernel index out of range. */
 mk_status mk_module_info(const mk_module* m, mk_module_info_t* info);
 mk_status mk_subkernel_info(const mk_module* m, int32_t i, mk_subkernel_info_t* info);
 
@@ -163,9 +179,17 @@ mk_status mk_subkernel_info(const mk_module* m, int32_t i, mk_subkernel_info_t* 
  * test-only mutant id).  MK_E_UNSUPPORTED if the family has no such impl. */
 mk_status mk_subkernel_select(mk_module* m, int32_t i, int32_t impl_id);
 
+/* Bytes of device workspace mk_run needs for this module under any of its
+ * subkernels' implementations: the materialised intermediates of the chosen
+ * decomposition (the tensors the top-level module passes between subproblems,
+ * Sec. 3 and App. H.1) followed by the largest scratch of any subkernel.
+ * The caller allocates it (the top-level wrapper allocates and launches,
+ * App. I.2).  Host only. */
 mk_status mk_workspace_size(const mk_module* m, int64_t* bytes);
 
-/* Enqueue the composition on `stream`.  dev_inputs[n_inputs] are device
+/* Enqueue the composition on `stream`: the top-level module S calling its
+ * subproblem kernels in order (Sec. 3; App. H.1 shows such an S for a CvT
+ * block).  dev_inputs[n_inputs] are device
  * pointers to the module inputs, dev_out receives the module output, dev_ws is
  * a device workspace of ws_bytes >= mk_workspace_size.  Returns after
  * enqueueing, unless per_subkernel_ms is non-NULL: then each subkernel is
@@ -175,7 +199,8 @@ mk_status mk_run(mk_module* m, const void* const* dev_inputs, void* dev_out, voi
                  int64_t ws_bytes, void* stream, float* per_subkernel_ms);
 
 /* Launch-level profiling (timing of each kernel launch, for roofline
- * figures).  While a profile is open, every mk_run of the module also brackets
+ * figures; Sec. 4 times kernels with HIP / CUDA events over repeated runs
+ * after warm-up).  While a profile is open, every mk_run of the module also brackets
  * each of its kernel launches with HIP events, without synchronising, until
  * max_launches launches are recorded (later launches are not recorded).
  * mk_profile_end synchronises on the last recorded launch, writes the elapsed
@@ -219,9 +244,12 @@ typedef struct {
   mk_check_result results[MK_MAX_CHECKS];
 } mk_verify_report;
 
-/* Poison the workspace with NaN bytes, run the module once (as mk_run),
- * synchronise, copy each checked stage to the host and compare.  Returns MK_OK
- * when the checks ran; pass/fail is in *report.  n_checks <= MK_MAX_CHECKS. */
+/* The verifier (Sec. 3, "Evaluate"; per stage as in App. D's decomposed
+ * checking).  Poison the workspace and the output buffer with NaN bytes (0xFF), run the
+ * module once (as mk_run), synchronise, copy each checked stage to the host
+ * and compare: an element that no kernel wrote reads back as NaN and fails.
+ * Returns MK_OK when the checks ran; pass/fail is in *report.
+ * n_checks <= MK_MAX_CHECKS. */
 mk_status mk_verify(mk_module* m, const void* const* dev_inputs, void* dev_out, void* dev_ws,
                     int64_t ws_bytes, void* stream, int32_t n_checks, const mk_check* checks,
                     mk_verify_report* report);
@@ -259,6 +287,24 @@ mk_status mk_swap(mk_module* m, const void* const* dev_inputs, void* dev_out, vo
 mk_status mk_budget_shares(int32_t n, const float* ms, const int32_t* needs_work,
                            float* shares);
 
+/* Seeded synthetic inputs: fill host_dst with elements 0 .. n-1 of input
+ * tensor `tensor_id` under `seed`, drawn from N(p0, p1) (dist 0; p1 is the
+ * standard deviation) or U(p0, p1) (dist 1), rounded to float32 and, for
+ * MK_BF16, to bfloat16 (raw 16-bit patterns), both to nearest even.  The
+ * generator is counter based (SplitMix64 mixing, Steele, Lea and Flood,
+ * OOPSLA 2014; Box-Muller cosine branch), so element i does not depend on n
+ * or on the thread count.  It replaces the fixed-seed input rule of the
+ * kernel-generation prompt (App. I.1, "SUBKERNEL INPUT FUNCTION
+ * REQUIREMENTS") with per-tensor streams, and its bytes are exactly those of
+ * the stand-alone generator the tests feed to the reference evaluation.
+ * host_dst is caller-owned host memory of n floats or n uint16.
+ * MK_E_INVALID_ARG on a null host_dst with n > 0, n < 0 or an unknown dist;
+ * MK_E_DTYPE on an unknown dtype. */
+mk_status mk_gen_fill(uint64_t seed, int32_t tensor_id, int32_t dist, double p0, double p1,
+                      int32_t dtype, void* host_dst, int64_t n);
+
+/* Status names and the calling thread's last error message (a static or
+ * thread-local string; never NULL). */
 const char* mk_status_str(mk_status s);
 const char* mk_last_error(void);
 

@@ -4,6 +4,7 @@ A module is a plain dict {"dtype": "f32"|"bf16", "inputs": [shape, ...],
 "ops": [{"kind": name, "in": [...], "ip": [...], "fp": [...]}, ...]}; inputs
 are flat numpy arrays of the storage type (float32, or uint16 bfloat16 bits).
 """
+import contextlib
 import ctypes
 import os
 import subprocess
@@ -49,13 +50,30 @@ class _Plan(ctypes.Structure):
                 ("alg_bytes", ctypes.c_int64)]
 
 
-def build():
-    """Compile libmko.so with gcc (plain C99, OpenMP)."""
-    src = os.path.join(_HERE, "mko.c")
-    tmp = _LIB + ".tmp"
+SOURCE = os.path.join(_HERE, "mko.c")
+
+
+def build(src=SOURCE, out=None):
+    """Compile the oracle with gcc (plain C99, OpenMP): libmko.so from mko.c by
+    default; tests that plant a mistake in a copy of mko.c build that copy."""
+    out = out or _LIB
+    tmp = out + ".tmp"
     subprocess.check_call(["gcc", "-O2", "-std=c99", "-D_DEFAULT_SOURCE", "-fPIC", "-shared",
-                           "-fopenmp", "-Wall", "-o", tmp, src, "-lm"])
-    os.replace(tmp, _LIB)
+                           "-fopenmp", "-Wall", "-I", _HERE, "-o", tmp, src, "-lm"])
+    os.replace(tmp, out)
+
+
+@contextlib.contextmanager
+def library(path):
+    """Evaluate with another build of the oracle inside the block (used by the
+    tests that show a pin rejects a planted mistake)."""
+    global _lib, _LIB
+    saved = (_lib, _LIB)
+    _lib, _LIB = None, path
+    try:
+        yield
+    finally:
+        _lib, _LIB = saved
 
 
 def _load():

@@ -1,6 +1,7 @@
 """Build the native libraries in-tree for gfx950.
 
-libmk.so      the composed-module library (HIP kernels + C ABI), via hipcc
+libmk.so      the composed-module library (HIP kernels + C ABI, with the input
+              generator linked in for mk_gen_fill), via hipcc
 libmkgen.so   the seeded input generator (plain C, gcc)
 
 Objects go to _build/ (git-ignored); every source is recompiled on each call.
@@ -40,10 +41,19 @@ def _compile(src):
     return obj
 
 
+def _compile_gen():
+    """The input generator (plain C) linked into libmk.so for mk_gen_fill."""
+    obj = os.path.join(BUILD, "mkgen.c.o")
+    subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-Wall", "-Wno-unknown-pragmas", "-c",
+                           os.path.join(PKG, "inputs", "mkgen.c"), "-o", obj])
+    return obj
+
+
 def build_libmk(jobs=8):
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(jobs) as ex:
         objs = list(ex.map(_compile, _sources()))
+    objs.append(_compile_gen())
     out = os.path.join(PKG, "libmk.so")
     tmp = out + ".tmp"
     subprocess.check_call([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs)

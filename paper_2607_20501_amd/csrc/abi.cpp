@@ -383,10 +383,17 @@ mk_status mk_verify(mk_module* m, const void* const* dev_inputs, void* dev_out, 
     if (s != MK_OK) return s;
     hipStream_t st = (hipStream_t)stream;
     const int64_t ws = ws_total(p);
-    // NaN bytes in every intermediate and scratch byte: a subkernel that reads
-    // something no earlier subkernel wrote produces NaN.
+    // NaN bytes in every intermediate and scratch byte and in the output: a
+    // subkernel that reads something no earlier subkernel wrote produces NaN,
+    // and output elements no kernel writes stay NaN (rather than holding an
+    // earlier run's values).
     if (ws > 0) {
       hipError_t e = hipMemsetAsync(dev_ws, 0xFF, (size_t)ws, st);
+      if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    }
+    {
+      const int64_t out_bytes = mk::numel(p.vshape.back()) * mk::elem_size(p.dtype);
+      hipError_t e = hipMemsetAsync(dev_out, 0xFF, (size_t)out_bytes, st);
       if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
     }
     s = mk_run(m, dev_inputs, dev_out, dev_ws, ws_bytes, stream, nullptr);

@@ -5,8 +5,10 @@
 // touching the others (MKEvolve Sec. 3, "Swap").  Ids >= 100 are test-only
 // mutants reproducing the eleven injected bugs of App. D (five attention,
 // six FFN; the tile-boundary and accumulator bugs serve both blocks), used to
-// show that per-stage verification catches them.  Mutants run on the simple
-// kernels, except the epilogue-chain ones, which rewrite the chain.
+// show that per-stage verification catches them, plus one that leaves an
+// output row unwritten (the verifier must not pass on stale output bytes).
+// Mutants run on the simple kernels, except the epilogue-chain ones, which
+// rewrite the chain.
 #include "impls.hpp"
 
 #include <algorithm>
@@ -25,7 +27,8 @@ enum Mutant : int32_t {
   MUT_UNSAFE_LAYERNORM = 106,   // rows scaled by 1/sigma without subtracting the mean
   MUT_GELU_SIGMOID = 107,       // x * sigmoid(1.702 x) instead of exact GELU
   MUT_NO_RESIDUAL = 108,        // residual add dropped
-  MUT_RELU_FOR_GELU = 109       // ReLU instead of GELU
+  MUT_RELU_FOR_GELU = 109,      // ReLU instead of GELU
+  MUT_SKIP_LAST_ROW = 110       // a row kernel that leaves its last output row unwritten
 };
 
 static bool chain_has(const EpiChain& c, int code) {
@@ -75,6 +78,8 @@ bool impl_exists(const Plan& p, const Subkernel& sk, int impl) {
       return c && chain_has_gelu(*c);
     case MUT_NO_RESIDUAL:
       return c && chain_has(*c, EPI_ADD);
+    case MUT_SKIP_LAST_ROW:
+      return sk.family == MK_FAM_ROW && sk.row.rows > 1;
     default:
       return false;
   }
@@ -238,7 +243,7 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       RowArgs a{};
       a.x = vals[r.x_value];
       a.y = out;
-      a.rows = r.rows;
+      a.rows = impl == MUT_SKIP_LAST_ROW ? r.rows - 1 : r.rows;
       a.len = r.len;
       a.op = r.op;
       a.gamma = r.g_value >= 0 ? vals[r.g_value] : nullptr;

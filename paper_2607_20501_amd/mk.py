@@ -84,7 +84,7 @@ class mk_verify_report(ctypes.Structure):
 EXPORTS = ["mk_decomposition_preset", "mk_module_create", "mk_module_destroy", "mk_module_info",
            "mk_subkernel_info", "mk_subkernel_select", "mk_workspace_size", "mk_run",
            "mk_verify", "mk_status_str", "mk_last_error", "mk_profile_begin", "mk_profile_end",
-           "mk_swap_decide", "mk_swap", "mk_budget_shares"]
+           "mk_swap_decide", "mk_swap", "mk_budget_shares", "mk_gen_fill"]
 
 _lib = None
 
@@ -125,6 +125,10 @@ def load():
     lib.mk_budget_shares.argtypes = [ctypes.c_int32, fp, ip, fp]
     for f in ("mk_swap_decide", "mk_swap", "mk_budget_shares"):
         getattr(lib, f).restype = ctypes.c_int
+    lib.mk_gen_fill.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32,
+                                ctypes.c_double, ctypes.c_double, ctypes.c_int32, vp,
+                                ctypes.c_int64]
+    lib.mk_gen_fill.restype = ctypes.c_int
     lib.mk_status_str.argtypes = [ctypes.c_int]
     lib.mk_status_str.restype = ctypes.c_char_p
     lib.mk_last_error.argtypes = []
@@ -272,6 +276,16 @@ def mk_verify(h, dev_inputs, dev_out, dev_ws, ws_bytes, stream, checks):
             "results": res}
 
 
+def mk_gen_fill(seed, tensor_id, dist, p0, p1, dtype, n):
+    """Elements 0..n-1 of seeded input tensor `tensor_id` (numpy float32, or
+    uint16 bfloat16 bit patterns for dtype 'bf16')."""
+    bf = dtype in ("bf16", 1)
+    out = np.empty(int(n), dtype=np.uint16 if bf else np.float32)
+    _check(load().mk_gen_fill(int(seed), int(tensor_id), int(dist), float(p0), float(p1),
+                              1 if bf else 0, out.ctypes.data_as(ctypes.c_void_p), int(n)))
+    return out
+
+
 def mk_swap_decide(ms_selected, ms_reference, tau):
     """-> (swap flags, triggered) for per-subkernel times (host lists)."""
     n = len(ms_selected)
@@ -387,9 +401,10 @@ def device_buffers(module, host_inputs, ws_bytes, device="cuda"):
 
 
 def out_tensor(module, out_shape, device="cuda"):
+    """Output buffer filled with NaN, so elements a run leaves unwritten show."""
     import torch
     dt = torch.bfloat16 if module["dtype"] == "bf16" else torch.float32
-    return torch.empty(out_shape, dtype=dt, device=device)
+    return torch.full(out_shape, float("nan"), dtype=dt, device=device)
 
 
 def to_float64(t):

@@ -96,3 +96,30 @@ def test_ragged_element_wise_tail():
               "ops": [op("BIAS", [0, 1]), op("GELU_TANH", [2])]}
     for dec in ("fused", "split"):
         check(module, dec)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_verify_rejects_an_unwritten_output_row(dtype):
+    """mk_verify poisons the output buffer: a final-stage kernel that leaves
+    its last row unwritten fails, even when the buffer already holds a
+    correct output from an earlier run of the same module."""
+    from paper_2607_20501_amd import inputs
+    import oracle
+    from helpers import TOL
+    module = workloads.gemm_gelu_softmax(M=70, K=64, N=300, dtype=dtype)
+    groups = mk.mk_decomposition_preset(module, "split")
+    host = inputs.make_inputs(module, 0)
+    ref = oracle.run(module, groups, host, keep={len(groups) - 1})[-1]
+    m = mk.Module(module, groups)
+    ins, _, ws = mk.device_buffers(module, host, m.workspace_size())
+    out = mk.out_tensor(module, m.info["out_shape"])
+    rtol, atol = TOL[dtype]
+    checks = [{"stage": m.n - 1, "expect": ref.reshape(-1), "rtol": rtol, "atol": atol}]
+    assert m.verify(ins, out, ws, checks)["pass"]
+    m.run(ins, out, ws)                      # a correct output now sits in `out`
+    torch.cuda.synchronize()
+    m.select(m.n - 1, 110)                   # the softmax rows kernel skips the last row
+    rep = m.verify(ins, out, ws, checks)
+    assert not rep["pass"]
+    r = rep["results"][0]
+    assert r["n_nonfinite"] == 300 and r["worst_index"] >= 69 * 300, describe(rep)

@@ -42,3 +42,18 @@ def test_make_inputs_shapes():
     xs = inputs.make_inputs(m, 0)
     assert [a.size for a in xs] == [128 * 256, 256 * 256, 256]
     assert all(a.dtype == np.float32 for a in xs)
+
+
+def test_library_mk_gen_fill_gives_the_generator_bytes():
+    """libmk's mk_gen_fill is the same generator the tests feed to the oracle."""
+    from paper_2607_20501_amd import mk
+    for dtype in ("f32", "bf16"):
+        for dist, p0, p1 in ((inputs.NORMAL, 0.0, 0.02), (inputs.UNIFORM, -0.1, 0.1)):
+            a = mk.mk_gen_fill(5, 2, dist, p0, p1, dtype, 4097)
+            b = inputs.fill(5, 2, dist, p0, p1, dtype, 4097)
+            np.testing.assert_array_equal(a, b)
+    assert mk.mk_gen_fill(0, 0, inputs.NORMAL, 0.0, 1.0, "f32", 0).size == 0
+    import pytest
+    with pytest.raises(mk.MkError) as e:
+        mk.mk_gen_fill(0, 0, 7, 0.0, 1.0, "f32", 4)
+    assert e.value.status == 1

@@ -439,3 +439,130 @@ def test_plan_materialisation_rule():
         oracle.plan(x, [0, 0, 1])          # op 0's output read by op 2 outside its group
     oracle.plan(x, [0, 1, 2])
     oracle.plan(x, [0, 0, 0])
+
+
+# --------------------------------------------------------------------------- channel bias
+
+def check_bias_channel():
+    """Per-channel bias of an NCHW tensor: on a zero input every position of
+    channel c holds b[c] (a non-square image with three distinct biases, so a
+    bias indexed by position or by the flat index modulo C differs), and the
+    conv + channel bias chain equals torch's conv2d with its own bias argument
+    in float64, grouped with the conv and split from it."""
+    N, C, H, W = 2, 3, 2, 5
+    b = np.array([1.0, 10.0, 100.0])
+    m = module("f32", [(N, C, H, W), (C,)], [op("BIAS_CHANNEL", [0, 1])])
+    got = run1(m, f32_inputs(np.zeros((N, C, H, W)), b))[0]
+    for c in range(C):
+        assert (got[:, c] == b[c]).all(), (c, got[:, c])
+    rng = np.random.default_rng(21)
+    n, ci, h, w_, k = 2, 3, 5, 7, 4
+    x = rng.standard_normal((n, ci, h, w_)).astype(np.float32)
+    wt = rng.standard_normal((k, ci, 3, 3)).astype(np.float32)
+    bias = (rng.standard_normal(k) * 3).astype(np.float32)
+    conv = module("f32", [(n, ci, h, w_), (k, ci, 3, 3), (k,)],
+                  [op("CONV2D", [0, 1], [1, 1]), op("BIAS_CHANNEL", [3, 2])])
+    ref = torch.nn.functional.conv2d(torch.from_numpy(x.astype(np.float64)),
+                                     torch.from_numpy(wt.astype(np.float64)),
+                                     torch.from_numpy(bias.astype(np.float64)),
+                                     stride=1, padding=1).numpy()
+    for groups in ([0, 0], [0, 1]):
+        y = oracle.run(conv, groups, f32_inputs(x, wt, bias), ideal=True)[-1]
+        np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_bias_channel_hand_values_and_torch_conv_bias():
+    check_bias_channel()
+
+
+# --------------------------------------------------------------------------- composition
+
+def tiny_modules(dtype):
+    from paper_2607_20501_amd import workloads
+    return [
+        workloads.linear_relu_rowsum(M=5, K=7, N=6, dtype=dtype),
+        workloads.gemm_gelu_softmax(M=4, K=6, N=9, dtype=dtype),
+        workloads.conv_relu_gap(N=2, C=3, H=5, W=4, K=4, dtype=dtype),
+        workloads.mlp_block(M=3, D=8, F=12, dtype=dtype),
+        workloads.transformer_layer(B=2, S=5, D=8, H=2, F=12, dtype=dtype),
+    ]
+
+
+def all_groupings(n):
+    for cuts in range(1 << (n - 1)):
+        g = [0]
+        for i in range(n - 1):
+            g.append(g[-1] + ((cuts >> i) & 1))
+        yield g
+
+
+def check_composition(dtype):
+    """Sec. 3 / App. H.1: a top-level module that chains subproblem kernels
+    computes the module itself, whatever the grouping.  For every contiguous
+    grouping the oracle accepts (brute force over all 2^(n-1)), the output
+    equals the all-split grouping's within the dtype tolerance (plus the
+    row-scaled softmax check), and without the rounding model the output does
+    not depend on the grouping at all."""
+    from paper_2607_20501_amd import inputs
+    rtol, atol = {"f32": (1e-4, 1e-5), "bf16": (2e-2, 2e-2)}[dtype]
+    for m in tiny_modules(dtype):
+        n = len(m["ops"])
+        host = inputs.make_inputs(m, 3)
+        split = list(range(n))
+        ref = oracle.run(m, split, host, keep={n - 1})[-1]
+        ideal = oracle.run(m, split, host, ideal=True, keep={n - 1})[-1]
+        atol_out = atol / ref.shape[-1] if m["ops"][-1]["kind"] == "SOFTMAX" else atol
+        accepted = 0
+        for g in all_groupings(n):
+            try:
+                oracle.plan(m, g)
+            except ValueError:
+                continue
+            accepted += 1
+            got = oracle.run(m, g, host, keep={n - 1})[-1]
+            np.testing.assert_allclose(got, ref, rtol=rtol, atol=atol_out,
+                                       err_msg=f"{m['name']} grouping {g}")
+            np.testing.assert_array_equal(
+                oracle.run(m, g, host, ideal=True, keep={n - 1})[-1], ideal)
+        assert accepted >= n, (m["name"], accepted)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_every_grouping_agrees_with_all_split(dtype):
+    check_composition(dtype)
+
+
+# --------------------------------------------------------------------------- planted mistakes
+
+def planted(tmp_path, old, new):
+    """A copy of the oracle with one plausible mistake planted in its source
+    (CPU only); returns the context that evaluates with it."""
+    src = open(mko.SOURCE).read()
+    assert src.count(old) == 1, old
+    path = tmp_path / "mko_planted.c"
+    path.write_text(src.replace(old, new))
+    so = str(tmp_path / "libmko_planted.so")
+    mko.build(str(path), so)
+    return oracle.library(so)
+
+
+def test_bias_channel_pin_rejects_flat_index_bias(tmp_path):
+    with planted(tmp_path, "b[(k / hw) % C]", "b[k % C]"):
+        with pytest.raises(AssertionError):
+            check_bias_channel()
+
+
+def test_bias_channel_pin_rejects_position_index_bias(tmp_path):
+    with planted(tmp_path, "b[(k / hw) % C]", "b[(k % hw) % C]"):
+        with pytest.raises(AssertionError):
+            check_bias_channel()
+
+
+def test_composition_pin_rejects_rounding_to_the_wrong_dtype(tmp_path):
+    # Group outputs of an fp32 module rounded to bfloat16: the result then
+    # depends on where the groups end.
+    with planted(tmp_path, "if (is_last || ln_prologue) round_to(y, n, d->dtype);",
+                 "if (is_last || ln_prologue) round_to(y, n, MKO_BF16);"):
+        with pytest.raises(AssertionError):
+            check_composition("f32")
+
