@@ -3,14 +3,17 @@
 
 A step is one run of the whole composed module (every subkernel of the
 chosen decomposition) over one batch of synthetic, seeded input that is
-already resident in HBM.  Default workload: the bf16 module
-x[8192,4096] @ W[4096,4096] + b, tanh-GELU, scale 0.5, row softmax, fused.
+already resident in HBM.  Default workload: the bf16 transformer MLP block
+x[16384,4096] -> LayerNorm -> Linear 4096->14336 -> exact GELU -> Linear
+14336->4096 -> + x, fused (the largest of the five workloads); --config
+selects the others.
 
 Prints ONE JSON line with the throughput of the fused composition (TFLOP/s of
 the module's algorithmic flops), the split composition beside it, the
 roofline of the dominant kernel (from HIP events around each launch, recorded
-live over the timed steps) and the oracle's CPU throughput on a bounded row
-sample (which also checks those rows of the GPU output).
+live over the timed steps) and the oracle's CPU throughput on a bounded
+sample of independent units -- rows, images or sequences -- which also checks
+those units of the GPU output).
 """
 import argparse
 import hashlib
@@ -93,7 +96,8 @@ def measured_traffic(workload, kernel):
         return None
     with open(path) as fh:
         table = json.load(fh)
-    rec = table.get(workload, {}).get(kernel)
+    rec = table.get(workload, {})
+    rec = rec.get(kernel) or rec.get(kernel.split(" ")[0])
     if not rec or rec.get("source_digest") != source_digest(GEMM_SOURCES):
         return None
     return rec["hbm_bytes_per_launch"]
@@ -143,33 +147,71 @@ def median_flushed(mod, ins, out, ws, runs, flush):
     return statistics.median(a.elapsed_time(b) for a, b in ev)
 
 
-def cpu_baseline(module, host, rows, out_dev):
-    """The oracle on the first `rows` rows of a row-independent module; also
-    compares those rows of the GPU output."""
+TOL = {"f32": (1e-4, 1e-5), "bf16": (2e-2, 2e-2)}
+
+
+def sample_module(module, n):
+    """The same module over n independent units of its leading dimension
+    (rows of a row-wise module, images of the conv module, sequences of the
+    transformer layer): the first input's leading size and the batch
+    parameter of attention ops become n."""
+    sub = json.loads(json.dumps(module))
+    sub["inputs"][0][0] = n
+    for o in sub["ops"]:
+        if o["kind"] in ("QK", "PV"):
+            o["ip"][0] = n
+    return sub
+
+
+def cpu_baseline(module, host, units, out_dev, unit_name):
+    """The oracle on the units `units` of the leading dimension (each unit is
+    independent of the others), timed on the host cores; also compares those
+    units of the GPU output element by element at the module dtype's
+    tolerance (softmax outputs also against atol / row length)."""
     import numpy as np
     import oracle
     from paper_2607_20501_amd import mk
-    sub = json.loads(json.dumps(module))
-    M = module["inputs"][0][0]
-    rows = min(rows, M)
-    sub["inputs"][0][0] = rows
-    K = module["inputs"][0][1]
-    sub_host = [host[0][:rows * K]] + list(host[1:])
+    n_all = module["inputs"][0][0]
+    per = int(np.prod(module["inputs"][0][1:]))
+    sub = sample_module(module, len(units))
+    sub_host = [np.concatenate([host[0][u * per:(u + 1) * per] for u in units])] + list(host[1:])
     groups = mk.mk_decomposition_preset(module, "fused")
-    threads = os.cpu_count() or 1
+    threads = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
     t = time.perf_counter()
     ref = oracle.run(sub, groups, sub_host, keep={len(module["ops"]) - 1}, nthreads=threads)[-1]
     dt = time.perf_counter() - t
     flops = oracle.plan(sub, groups)["flops"]
-    got = mk.to_float64(out_dev[:rows])
+    import torch
+    got = mk.to_float64(out_dev[torch.tensor(units, device=out_dev.device)])
+    rtol, atol = TOL[module["dtype"]]
     err = np.abs(got - ref)
-    tol = 2e-2 * np.abs(ref) + 2e-2 / ref.shape[-1]
+    ok = err <= atol + rtol * np.abs(ref)
+    if module["ops"][-1]["kind"] == "SOFTMAX":
+        ok &= err <= atol / ref.shape[-1] + rtol * np.abs(ref)
+    span = (f"units {units[0]}..{units[-1]}" if units == list(range(units[0], units[-1] + 1))
+            else "units " + ",".join(map(str, units)))
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {rows} of {M} rows of the same fused module (fp64 oracle, "
-                      f"{flops / 1e9:.1f} GFLOP in {dt:.1f} s)",
+            "sample": f"{len(units)} of {n_all} {unit_name} ({span.replace('units', unit_name)})"
+                      f" of the same fused module (fp64 oracle, {flops / 1e9:.1f} GFLOP in "
+                      f"{dt:.1f} s)",
             "seconds": dt,
-            "parity_rows_checked": rows, "parity_max_abs_err": float(err.max()),
-            "parity_pass": bool((err <= tol).all())}
+            "parity_units_checked": len(units), "parity_max_abs_err": float(err.max()),
+            "parity_pass": bool(ok.all())}
+
+
+def baseline_units(cfg, module, flops, cpu_units):
+    """Which units the oracle leg evaluates: about 800 GFLOP of rows (row-wise
+    modules), every image (conv, 118 GFLOP), the first and the last sequence
+    (transformer, 223 GFLOP each)."""
+    n = module["inputs"][0][0]
+    if cfg == 3:
+        k = cpu_units or n
+        return list(range(min(k, n))), "images"
+    if cfg == 5:
+        k = cpu_units or 2
+        return (list(range(k - 1)) + [n - 1]) if k < n else list(range(n)), "sequences"
+    k = cpu_units or max(1, min(n, int(800e9 / (flops / n))))
+    return list(range(min(k, n))), "rows"
 
 
 def main():
@@ -177,12 +219,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--dtype", default=None, choices=[None, "f32", "bf16"])
     ap.add_argument("--decomp", default="fused", choices=["fused", "split"])
     ap.add_argument("--no-split", action="store_true", help="skip timing the split form")
-    ap.add_argument("--cpu-rows", type=int, default=None,
-                    help="rows of the oracle sample (default: about 300 GFLOP of work)")
+    ap.add_argument("--cpu-units", type=int, default=None,
+                    help="units of the oracle sample: rows, images or sequences (default: "
+                         "about 800 GFLOP of rows, every image, first and last sequence)")
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
                     help="run one plain device copy of this size first (counter calibration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -272,7 +315,7 @@ def main():
         peak = PEAK_BF16_TFLOPS if bf else PEAK_F32_TFLOPS
         roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                 "frac": achieved / peak,
-                "traffic": measured_traffic(module["name"], names[k].split(" ")[0])}
+                "traffic": measured_traffic(module["name"], names[k])}
     else:
         achieved = sub["alg_bytes"] / (per_launch[k] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -302,10 +345,9 @@ def main():
         "launch_us": [round(x * 1e3, 2) for x in per_launch],
     }
     line.update(result)
-    if not args.no_cpu_baseline and args.config in (1, 2, 4):
-        M = module["inputs"][0][0]
-        rows = args.cpu_rows or max(1, min(M, int(300e9 / (flops / M))))
-        line["cpu_baseline"] = cpu_baseline(module, host, rows, out)
+    if not args.no_cpu_baseline:
+        units, unit_name = baseline_units(args.config, module, flops, args.cpu_units)
+        line["cpu_baseline"] = cpu_baseline(module, host, units, out, unit_name)
     print(json.dumps(line), flush=True)
 
 

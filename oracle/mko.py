@@ -12,7 +12,8 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB = os.path.join(_HERE, "libmko.so")
+# MKO_LIBRARY names another build of the oracle (the sanitized build).
+_LIB = os.environ.get("MKO_LIBRARY") or os.path.join(_HERE, "libmko.so")
 _lib = None
 
 KINDS = ["GEMM", "BIAS", "BIAS_CHANNEL", "RELU", "GELU_ERF", "GELU_TANH", "SCALE", "ADD",
