@@ -198,6 +198,21 @@ mk_status mk_workspace_size(const mk_module* m, int64_t* bytes);
 mk_status mk_run(mk_module* m, const void* const* dev_inputs, void* dev_out, void* dev_ws,
                  int64_t ws_bytes, void* stream, float* per_subkernel_ms);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): mk_run with
+ * no workspace argument.  The workspace is a static device array of
+ * MK_NOALLOC_WS_BYTES owned by the library; each device the library runs on
+ * holds its own copy until the process ends (its address is looked up on the
+ * first call on that device).  The caller still passes the inputs and the
+ * output; the call only enqueues, allocates no device memory and creates no
+ * events.  Every call on one device shares that device's array, which keeps
+ * the last call's contents: calls that overlap on one device (two streams, two
+ * threads) race and must be serialised by the caller.  MK_E_WORKSPACE if
+ * mk_workspace_size exceeds MK_NOALLOC_WS_BYTES; other errors as for mk_run. */
+#define MK_NOALLOC_WS_BYTES (64ll << 20)
+mk_status mk_run_noalloc(mk_module* m, const void* const* dev_inputs, void* dev_out,
+                         void* stream);
+
 /* Launch-level profiling (timing of each kernel launch, for roofline
  * figures; Sec. 4 times kernels with HIP / CUDA events over repeated runs
  * after warm-up).  While a profile is open, every mk_run of the module also brackets

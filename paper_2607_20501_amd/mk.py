@@ -86,7 +86,8 @@ class mk_verify_report(ctypes.Structure):
 EXPORTS = ["mk_decomposition_preset", "mk_module_create", "mk_module_destroy", "mk_module_info",
            "mk_subkernel_info", "mk_subkernel_select", "mk_workspace_size", "mk_run",
            "mk_verify", "mk_status_str", "mk_last_error", "mk_profile_begin", "mk_profile_end",
-           "mk_swap_decide", "mk_swap", "mk_budget_shares", "mk_gen_fill"]
+           "mk_swap_decide", "mk_swap", "mk_budget_shares", "mk_gen_fill", "mk_run_noalloc"]
+NOALLOC_WS_BYTES = 64 << 20   # MK_NOALLOC_WS_BYTES
 
 _lib = None
 
@@ -98,6 +99,14 @@ def load():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    # torch carries its own copy of the HIP runtime under the same soname;
+    # loaded first, it is the one libmk binds to.  Loaded after libmk, it
+    # would be a second runtime in the process, and libmk's own calls (device
+    # queries, events) would not see the devices torch's memory lives on.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.POINTER
     vp = ctypes.c_void_p
@@ -110,11 +119,12 @@ def load():
     lib.mk_subkernel_select.argtypes = [vp, ctypes.c_int32, ctypes.c_int32]
     lib.mk_workspace_size.argtypes = [vp, P(ctypes.c_int64)]
     lib.mk_run.argtypes = [vp, P(vp), vp, vp, ctypes.c_int64, vp, P(ctypes.c_float)]
+    lib.mk_run_noalloc.argtypes = [vp, P(vp), vp, vp]
     lib.mk_verify.argtypes = [vp, P(vp), vp, vp, ctypes.c_int64, vp, ctypes.c_int32,
                               P(mk_check), P(mk_verify_report)]
     for f in ("mk_decomposition_preset", "mk_module_create", "mk_module_info",
               "mk_subkernel_info", "mk_subkernel_select", "mk_workspace_size", "mk_run",
-              "mk_verify"):
+              "mk_run_noalloc", "mk_verify"):
         getattr(lib, f).restype = ctypes.c_int
     lib.mk_profile_begin.argtypes = [vp, ctypes.c_int32]
     lib.mk_profile_end.argtypes = [vp, P(ctypes.c_float), ctypes.c_int32, P(ctypes.c_int32)]
@@ -227,6 +237,12 @@ def mk_run(h, dev_inputs, dev_out, dev_ws, ws_bytes, stream, n_subkernels=None):
     ms = (ctypes.c_float * n_subkernels)() if n_subkernels else None
     _check(load().mk_run(h, ptrs, dev_out, dev_ws, int(ws_bytes), stream, ms))
     return list(ms) if ms is not None else None
+
+
+def mk_run_noalloc(h, dev_inputs, dev_out, stream):
+    """mk_run on the library's static workspace (no workspace argument)."""
+    ptrs = (ctypes.c_void_p * max(1, len(dev_inputs)))(*dev_inputs)
+    _check(load().mk_run_noalloc(h, ptrs, dev_out, stream))
 
 
 def mk_profile_begin(h, max_launches):
@@ -356,6 +372,10 @@ class Module:
                       ws.data_ptr() if ws is not None and ws.numel() else None,
                       ws.numel() * ws.element_size() if ws is not None else 0, st,
                       self.n if timing else None)
+
+    def run_noalloc(self, dev_inputs, out, stream=None):
+        st = stream.cuda_stream if stream is not None else _current_stream()
+        mk_run_noalloc(self.h, self._ptrs(dev_inputs), out.data_ptr(), st)
 
     def swap(self, dev_inputs, out, ws, reference_impl=IMPL_SIMPLE, tau=0.9, n_runs=5,
              stream=None):
