@@ -161,12 +161,19 @@ struct SliceLoader {
   static constexpr int CPR = RB / 16;                    // chunks per row
   static constexpr int LQ = ROWS * CPR / (64 * WAVES);   // loads per thread per stage
   static_assert(LQ * 64 * WAVES == ROWS * CPR, "stage must split evenly over the loads");
-  // A lane's successive loads are 64*WAVES/CPR rows apart, a multiple of 64,
-  // which leaves both swizzles unchanged: one logical chunk serves them all.
-  static_assert((64 * WAVES / CPR) % 64 == 0, "swizzle must repeat across a lane's loads");
+  // A lane's successive loads are RSTEP = 64*WAVES/CPR rows apart.  When that
+  // is a multiple of 64 both swizzles repeat and one logical chunk serves all
+  // of them; four waves with 128-byte rows (RSTEP 32) alternate between two
+  // chunks, which only the whole-stage form (issue_full: K a multiple of the
+  // stage depth, so no lane needs a K bound) accepts.
+  static constexpr int RSTEP = 64 * WAVES / CPR;
+  static constexpr bool kRepeat = RSTEP % 64 == 0;
+  static_assert(kRepeat || (RB == 128 && RSTEP == 32), "unsupported load geometry");
   __amdgpu_buffer_rsrc_t src;
   uint32_t voff[LQ];   // byte offset at k0 = 0, kOob if the row is out of range
-  int lchunk;          // logical 16-byte chunk of this lane's loads
+  uint32_t range;      // bytes covered by src
+  int lchunk;          // logical 16-byte chunk of this lane's loads (of load 0)
+  int wid;             // this wave's index (wave-uniform)
 
   __device__ __forceinline__ int first_row() const {
     return ((threadIdx.x >> 6) * 64 + (threadIdx.x & 63)) / CPR;
@@ -174,16 +181,37 @@ struct SliceLoader {
   __device__ __forceinline__ void set_chunk() {
     const int p = (threadIdx.x >> 6) * 64 + (threadIdx.x & 63);
     lchunk = (p % CPR) ^ swz<RB>(p / CPR);
+    wid = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  }
+  // logical chunk of load q (its row is first_row() + q * RSTEP)
+  __device__ __forceinline__ int chunk_of(int q) const {
+    if constexpr (kRepeat) return lchunk;
+    const int p = (threadIdx.x >> 6) * 64 + (threadIdx.x & 63);
+    return (p % CPR) ^ swz<RB>(p / CPR + q * RSTEP);
   }
 
   __device__ __forceinline__ void init(const T* base, int64_t rows, int64_t ld, int64_t r0) {
+    range = (uint32_t)(rows * ld * (int64_t)sizeof(T));
     src = make_rsrc(base, rows * ld * (int64_t)sizeof(T));
     set_chunk();
 #pragma unroll
     for (int q = 0; q < LQ; ++q) {
-      const int64_t g = r0 + first_row() + q * (64 * WAVES / CPR);
-      voff[q] = g < rows ? (uint32_t)(g * ld * (int64_t)sizeof(T) + lchunk * 16) : kOob;
+      const int64_t g = r0 + first_row() + q * RSTEP;
+      voff[q] = g < rows ? (uint32_t)(g * ld * (int64_t)sizeof(T) + chunk_of(q) * 16) : kOob;
     }
+  }
+
+  // Loads Q0 .. Q1-1 of a whole stage into `dst` (this operand's slot), with
+  // the stage's uniform byte offset along K: every lane is inside K, and a
+  // stage past the last one passes soff = range, which puts every lane out of
+  // the descriptor's range (zeros; voff < 2^31 + 2^31 never wraps since the
+  // range is below 2 GB).
+  template <int Q0, int Q1>
+  __device__ __forceinline__ void issue_full(char* dst, uint32_t soff) const {
+#pragma unroll
+    for (int q = Q0; q < Q1; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * WAVES + wid) * 1024),
+                                               16, (int)voff[q], (int)soff, 0, 0);
   }
 
   // Rows gathered from arbitrary byte offsets (implicit-GEMM conv: output
@@ -191,11 +219,13 @@ struct SliceLoader {
   template <typename RowOff>
   __device__ __forceinline__ void init_gather(const T* base, int64_t bytes, int64_t rows,
                                               int64_t r0, RowOff rowoff) {
+    static_assert(kRepeat, "gathered rows need one chunk per lane");
+    range = (uint32_t)bytes;
     src = make_rsrc(base, bytes);
     set_chunk();
 #pragma unroll
     for (int q = 0; q < LQ; ++q) {
-      const int64_t g = r0 + first_row() + q * (64 * WAVES / CPR);
+      const int64_t g = r0 + first_row() + q * RSTEP;
       voff[q] = g < rows ? (uint32_t)(rowoff(g) + lchunk * 16) : kOob;
     }
   }
@@ -205,6 +235,7 @@ struct SliceLoader {
   // of wave w, lane i fills LDS chunk p = (q*WAVES + w)*64 + i, i.e. row
   // p/CPR, physical chunk p%CPR.
   __device__ __forceinline__ void issue(char* dst, int64_t k0, int64_t K, uint32_t soff) const {
+    static_assert(kRepeat, "a K bound per lane needs one chunk per lane");
     const int w = threadIdx.x >> 6;
     const bool in_k = lchunk * E < K - k0;
 #pragma unroll
@@ -219,6 +250,7 @@ struct SliceLoader {
   // Loads Q0 .. Q1-1 of the stage (plain rows): a stage's loads may be spread.
   template <int Q0, int Q1>
   __device__ __forceinline__ void issue_part(char* dst, int64_t k0, int64_t K) const {
+    static_assert(kRepeat, "a K bound per lane needs one chunk per lane");
     const int w = threadIdx.x >> 6;
     const bool in_k = lchunk * E < K - k0;
     const uint32_t soff = (uint32_t)(k0 * (int64_t)sizeof(T));
@@ -302,18 +334,20 @@ __device__ __forceinline__ void wait_vm() {
 // bank groups.
 constexpr int kSlabU = 65;
 
-// Copy acc[I] (rows I*32 .. I*32+31 of this wave's tile) into the slab.
-template <int I, int NJ>
+// Copy acc[I][J0], acc[I][J0+1] (rows I*32 .. I*32+31 of 64 of this wave's
+// columns) into the slab.
+template <int I, int NJ, int J0 = 0>
 __device__ __forceinline__ void stage_slab(const f32x16 (&acc)[4][NJ], float* slab, int lh,
                                            int lr) {
+  static_assert(J0 + 2 <= NJ, "a slab holds two column tiles");
 #pragma unroll
-  for (int j = 0; j < NJ; ++j)
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
       const int g = 2 * r4 + lh;
       *(f32x4*)(slab + (g * kSlabU + j * 32 + lr) * 4) =
-          f32x4{acc[I][j][4 * r4], acc[I][j][4 * r4 + 1], acc[I][j][4 * r4 + 2],
-                acc[I][j][4 * r4 + 3]};
+          f32x4{acc[I][J0 + j][4 * r4], acc[I][J0 + j][4 * r4 + 1], acc[I][J0 + j][4 * r4 + 2],
+                acc[I][J0 + j][4 * r4 + 3]};
     }
 }
 
@@ -545,11 +579,12 @@ __device__ __forceinline__ uint32_t conv_koff(const GemmArgs& a, int64_t k0) {
   return ((r * (uint32_t)a.cv_Wp + s) * C + c0) * (uint32_t)sizeof(T);
 }
 
-// LDS bytes of the epilogue: per wave a 32-row slab (8 row groups of kSlabU
-// 16-byte units), then the row-reduction exchange [WN][256 rows][2] floats.
-template <int WN, int BN>
+// LDS bytes of the epilogue: per wave SL 32-row slabs (8 row groups of
+// kSlabU 16-byte units), then the row-reduction exchange [WN][256 rows][2]
+// floats.
+template <int WN, int BN, int SL = 1>
 constexpr int epi_bytes() {
-  return 2 * WN * 8 * kSlabU * 16 + WN * BM * 2 * 4;
+  return SL * 2 * WN * 8 * kSlabU * 16 + WN * BM * 2 * 4;
 }
 
 // Variants: WN waves along N (2 rows of waves), BN columns per tile, STG
@@ -586,11 +621,18 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   // reuses the top of the LDS (clear of A0 and B0, which take the next tile's
   // stage 0 meanwhile).  Ring form: stage slots back to back, the epilogue
   // from 0.
-  static_assert(WTN == 64, "the epilogue maps 8 row groups x 8 column groups onto a wave");
+  static_assert(WTN == 64 || (PIPE == 3 && WTN == 128),
+                "the epilogue maps 8 row groups x 8 column groups onto 64 columns of a wave");
+  static_assert(PIPE != 3 || (!CONV && WN == 2 && BN == 256 && RB == 128 && sizeof(T) == 2 &&
+                              (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
+                               SIG == kSigBiasGeluTanhScale)),
+                "the four-wave form runs plain bf16 GEMMs with a compiled chain, no terminal");
   constexpr int kRing = PIPE ? 5 * 32768 : kStages * kStageBytes;
-  constexpr int kEpiOff = PIPE ? ((kRing - epi_bytes<WN, BN>()) & ~1023) : 0;
+  // (the four-wave epilogue alternates between two slabs per wave)
+  constexpr int kSlabs = PIPE == 3 ? 2 : 1;
+  constexpr int kEpiOff = PIPE ? ((kRing - epi_bytes<WN, BN, kSlabs>()) & ~1023) : 0;
   static_assert(PIPE == 0 || kEpiOff >= 65536, "the epilogue must leave A0 and B0 free");
-  constexpr int kEpiEnd = kEpiOff + epi_bytes<WN, BN>();
+  constexpr int kEpiEnd = kEpiOff + epi_bytes<WN, BN, kSlabs>();
   constexpr int kSmemMain = kEpiEnd > kRing ? kEpiEnd : kRing;
   // Conv: the tile's channel-bias values (first BIAS_CH step) after the ring.
   // Conv: the tile's channel-bias values (first BIAS_CH step): after the
@@ -639,7 +681,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   auto init_loaders = [&](const Item& it) {
     const int64_t m0 = row0_of(it), n0 = (int64_t)it.tc.tn * BN;
     la.init(A, it.sub < 0 ? a.M : min<int64_t>(a.M, m0 + SR), a.lda, m0);
-    if (CONV) {
+    if constexpr (CONV) {
       const int64_t bytes = a.cv_Hp * a.cv_Wp * a.cv_C * (int64_t)sizeof(T) *
                             ((uint32_t)a.N / (uint32_t)PQ);
       // 32-bit: positions and byte offsets in the padded input stay below
@@ -670,13 +712,17 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   };
   // Loads of stage ks (stages past the last read zeros: every lane's K bound
   // fails).
-  auto issue_a = [&](int ks) { la.issue(a_slot(ks), (int64_t)ks * BK, a.K); };
+  auto issue_a = [&](int ks) {
+    if constexpr (PIPE != 3) la.issue(a_slot(ks), (int64_t)ks * BK, a.K);
+  };
   auto issue_b = [&](int ks) {
-    const int64_t k0 = (int64_t)ks * BK;
-    if (CONV)
-      lb.issue(b_slot(ks), k0, a.K, conv_koff<T>(a, k0));
-    else
-      lb.issue(b_slot(ks), k0, a.K);
+    if constexpr (PIPE != 3) {
+      const int64_t k0 = (int64_t)ks * BK;
+      if (CONV)
+        lb.issue(b_slot(ks), k0, a.K, conv_koff<T>(a, k0));
+      else
+        lb.issue(b_slot(ks), k0, a.K);
+    }
   };
   // Sub-tile stages: A (its first 64 rows: one load per thread) in four 8 KB
   // slots at 0, B in four 32 KB slots from 32 KB, so stage 0 sits where a
@@ -684,12 +730,14 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   auto a_slot_s = [&](int ks) -> char* { return smem + (ks & 3) * 8192; };
   auto b_slot_s = [&](int ks) -> char* { return smem + 32768 + (ks & 3) * 32768; };
   auto issue_sub = [&](int ks) {
-    const int64_t k0 = (int64_t)ks * BK;
-    la.template issue_part<0, 1>(a_slot_s(ks), k0, a.K);
-    if (CONV)
-      lb.issue(b_slot_s(ks), k0, a.K, conv_koff<T>(a, k0));
-    else
-      lb.issue(b_slot_s(ks), k0, a.K);
+    if constexpr (PIPE != 3) {
+      const int64_t k0 = (int64_t)ks * BK;
+      la.template issue_part<0, 1>(a_slot_s(ks), k0, a.K);
+      if (CONV)
+        lb.issue(b_slot_s(ks), k0, a.K, conv_koff<T>(a, k0));
+      else
+        lb.issue(b_slot_s(ks), k0, a.K);
+    }
   };
 
   int v = next_item((int)blockIdx.x);
@@ -697,7 +745,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   Item it = item_of(v);
   TileCoord tc = it.tc;
   init_loaders(it);
-  if (!PIPE) {
+  if constexpr (!PIPE) {
 #pragma unroll
     for (int s = 0; s < kStages - 1; ++s)
       if (s < nk) {
@@ -743,7 +791,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
 
   // Row-reduction exchange [WN column groups][256 rows][2], after the slabs
   // (each wave's 32-row slab: 8 row groups of kSlabU 16-byte units).
-  float* red = (float*)(smem + kEpiOff) + WAVES * 8 * kSlabU * 4;
+  float* red = (float*)(smem + kEpiOff) + kSlabs * WAVES * 8 * kSlabU * 4;
   const int64_t cbase = a.c_off + bb * a.c_sb + hh * a.c_sh;
   T* C = (T*)a.C + cbase;
   constexpr int kTerm = sig_terminal(SIG);
@@ -764,8 +812,25 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   bool staged0 = false;   // this tile's stage 0 was issued during the last epilogue
   constexpr int kEpiVmem = (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
                             SIG == kSigBiasGeluTanhScale)
-                               ? 16
+                               ? 16 * (NJ / 2)
                                : 0;
+  // Four-wave form: LDS byte offsets of the A slots (stage ks in ks % 3) and
+  // B slots (ks % 2), and this lane's fragment address bases.  In a wave's
+  // 128 x 128 tile, fragment (i, kk) of A reads row rowbase + i*32 + lr,
+  // logical chunk 2kk + lh, whose physical chunk is (2kk ^ 4(i&1)) ^ X with
+  // X = lh ^ swz(lr) (rowbase and i*32 move the swizzle by 4(i&1) only):
+  // va[kk ^ 2(i&1)] + i*4096 within the slot (likewise B with j).
+  constexpr int kSlotA3[3] = {0, 65536, 98304};
+  constexpr int kSlotB3[2] = {32768, 131072};
+  uint32_t va3[4], vb3[4];
+  if constexpr (PIPE == 3) {
+    const int X = lh ^ swz<RB>(lr);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      va3[c] = (uint32_t)(rowbase * RB + lr * RB + (((2 * c) ^ X) << 4));
+      vb3[c] = (uint32_t)(colbase * RB + lr * RB + (((2 * c) ^ X) << 4));
+    }
+  }
   for (;;) {
     const int64_t m0 = row0_of(it), n0 = (int64_t)tc.tn * BN;
     const bool subt = CONV && PIPE && it.sub >= 0;
@@ -778,7 +843,107 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    if (PIPE && subt) {
+    if constexpr (PIPE == 3) {
+      // Four waves, one per SIMD, each a 128 x 128 quarter of the tile (4 x 4
+      // MFMA tiles); K a multiple of the 64-deep stage.  Same slot scheme as
+      // the eight-wave form (A of stage ks in slot ks % 3, B in ks % 2; A(ks+2)
+      // issued over sub-steps 0 and 1, B(ks+2) after the stage barrier, which
+      // sits before the last sub-step), with the stage loop unrolled by 6 so
+      // every slot offset is a constant: no address arithmetic per fragment
+      // read, no K-bound select per load (stages past the last read zeros via
+      // the stage offset).
+      auto soff3 = [&](int ks, uint32_t range) __attribute__((always_inline)) -> uint32_t {
+        return ks < nk ? (uint32_t)ks * RB : range;
+      };
+      auto read3 = [&](auto SA_, auto SB_, auto KK_, Frags<NJ, T>& f) __attribute__((always_inline)) {
+        constexpr int SA = decltype(SA_)::value, SB = decltype(SB_)::value;
+        constexpr int KK = decltype(KK_)::value;
+        typedef typename MfmaType<T>::frag F;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          f.a[i] = *(const F*)(smem + kSlotA3[SA] + i * 4096 + va3[KK ^ (2 * (i & 1))]);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          f.b[j] = *(const F*)(smem + kSlotB3[SB] + j * 4096 + vb3[KK ^ (2 * (j & 1))]);
+      };
+      // per sub-step: kMfmaSub MFMAs, kReadPairs pairs of fragment reads
+      auto interleave3 = [&](auto NV_) __attribute__((always_inline)) {
+        constexpr int nv = decltype(NV_)::value;
+#pragma unroll
+        for (int g = 0; g < kReadPairs; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
+        }
+#pragma unroll
+        for (int g = 0; g < nv; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfmaSub - kReadPairs - nv, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      Frags<NJ, T> f0, f1;
+      auto stage3 = [&](auto S6_, int ks) __attribute__((always_inline)) {
+        constexpr int S6 = decltype(S6_)::value;
+        constexpr int SA = S6 % 3, SB = S6 % 2, SA1 = (S6 + 1) % 3, SB1 = (S6 + 1) % 2,
+                      SA2 = (S6 + 2) % 3;
+        using I0 = std::integral_constant<int, 0>;
+        using I1 = std::integral_constant<int, 1>;
+        using I2 = std::integral_constant<int, 2>;
+        using I3 = std::integral_constant<int, 3>;
+        using CA = std::integral_constant<int, SA>;
+        using CB = std::integral_constant<int, SB>;
+        const uint32_t sa2 = soff3(ks + 2, la.range), sb2 = soff3(ks + 2, lb.range);
+        read3(CA{}, CB{}, I1{}, f1);
+        la.template issue_full<0, kA0>(smem + kSlotA3[SA2], sa2);
+        mfma_step<NJ, T, false>(f0, acc);
+        interleave3(std::integral_constant<int, kA0>{});
+        read3(CA{}, CB{}, I2{}, f0);
+        la.template issue_full<kA0, LA>(smem + kSlotA3[SA2], sa2);
+        mfma_step<NJ, T, false>(f1, acc);
+        interleave3(std::integral_constant<int, kA1>{});
+        read3(CA{}, CB{}, I3{}, f1);
+        mfma_step<NJ, T, false>(f0, acc);
+        interleave3(std::integral_constant<int, 0>{});
+        // stage ks+1 landed (only A(ks+2) may remain) and this wave's reads
+        // of stage ks are done; the barrier makes both hold for every wave
+        wait_vm<LA>();
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        read3(std::integral_constant<int, SA1>{}, std::integral_constant<int, SB1>{}, I0{}, f0);
+        lb.template issue_full<0, LB>(smem + kSlotB3[SB], sb2);
+        mfma_step<NJ, T, false>(f1, acc);
+        interleave3(std::integral_constant<int, LB>{});
+      };
+      if (!staged0) {
+        la.template issue_full<0, LA>(smem + kSlotA3[0], 0u);
+        lb.template issue_full<0, LB>(smem + kSlotB3[0], 0u);
+      }
+      la.template issue_full<0, LA>(smem + kSlotA3[1], soff3(1, la.range));
+      lb.template issue_full<0, LB>(smem + kSlotB3[1], soff3(1, lb.range));
+      if (staged0)
+        wait_vm<LA + LB + kEpiVmem>();
+      else
+        wait_vm<LA + LB>();
+      __builtin_amdgcn_s_barrier();
+      read3(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{},
+            std::integral_constant<int, 0>{}, f0);
+      int ks = 0;
+      for (; ks + 6 <= nk; ks += 6) {
+        stage3(std::integral_constant<int, 0>{}, ks);
+        stage3(std::integral_constant<int, 1>{}, ks + 1);
+        stage3(std::integral_constant<int, 2>{}, ks + 2);
+        stage3(std::integral_constant<int, 3>{}, ks + 3);
+        stage3(std::integral_constant<int, 4>{}, ks + 4);
+        stage3(std::integral_constant<int, 5>{}, ks + 5);
+      }
+      if (ks < nk) stage3(std::integral_constant<int, 0>{}, ks);
+      if (ks + 1 < nk) stage3(std::integral_constant<int, 1>{}, ks + 1);
+      if (ks + 2 < nk) stage3(std::integral_constant<int, 2>{}, ks + 2);
+      if (ks + 3 < nk) stage3(std::integral_constant<int, 3>{}, ks + 3);
+      if (ks + 4 < nk) stage3(std::integral_constant<int, 4>{}, ks + 4);
+    } else if (PIPE && subt) {
       // Row sub-tile: waves wm with wm*32 < SR compute rows wm*32 .. +31 of
       // it into acc[0]; every wave loads.  Three stages in flight; one
       // barrier per stage (it also orders the refill of the slot read in the
@@ -936,7 +1101,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     if (PIPE && more) {
       it_next = item_of(vn);
       init_loaders(it_next);
-      if (CONV && it_next.sub >= 0) {
+      if constexpr (PIPE == 3) {
+        la.template issue_full<0, LA>(smem + kSlotA3[0], 0u);
+        lb.template issue_full<0, LB>(smem + kSlotB3[0], 0u);
+      } else if (CONV && it_next.sub >= 0) {
         issue_sub(0);
       } else {
         issue_a(0);
@@ -960,7 +1128,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // the 8 lanes of a row (same rg) are lanes rg, rg+8, ..., rg+56.
     const int q = lane_e >> 3, rg = lane_e & 7;
     const int wn = wn_e;
-    float* slab = (float*)(smem + kEpiOff) + w_e * (8 * kSlabU * 4);
+    float* slab = (float*)(smem + kEpiOff) + w_e * (kSlabs * 8 * kSlabU * 4);
 
     // ---------------------------------------------------------------- epilogue
     // acc[i][j][r] is C[row, col] with
@@ -968,8 +1136,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // Each wave stages one 32-row slab at a time in its own LDS region; lane
     // (q, rg) then reads rows 4rg .. 4rg+3 of columns 8q .. 8q+7, applies the
     // chain to each row's 8 values and writes them with one 16-byte store.
-    const int64_t col0 = n0 + colbase + q * 8;
-    const int valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
+    // (the four-wave form finishes its 128 columns as two 64-column halves,
+    // moving col0 between them)
+    int64_t col0 = n0 + colbase + q * 8;
+    int valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
     // Conv: this lane's 8 positions lie in one image (PQ % 8 == 0).
     const int64_t img = CONV ? (int64_t)((uint32_t)col0 / (uint32_t)PQ) : 0;   // positions < 2^31
 
@@ -990,7 +1160,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // One row of the lane: values v of columns col0 .. col0+7 of tile row
     // lrow; `res` is its residual piece (kSigAdd, full pieces), `bt` the conv
     // channel bias of the row.
-    auto finish_row = [&](int lrow, float (&v)[8], const u32x4& res, float bt) {
+    auto finish_row = [&](int lrow, float (&v)[8], const u32x4& res, float bt) __attribute__((always_inline)) {
       const int64_t row = m0 + lrow;
       const bool row_ok = row < a.M;
       // Offset of (row, col0) in the output: row-major, or NCHW for a conv
@@ -1155,7 +1325,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
 
     // Residual pieces of this lane's 4 rows of slab i, as buffer loads (a
     // lane without a full piece reads zeros, with no branch to wait at).
-    auto load_res = [&](int i, u32x4 (&dst)[4]) {
+    auto load_res = [&](int i, u32x4 (&dst)[4]) __attribute__((always_inline)) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int64_t row = m0 + rowbase + i * 32 + rg * 4 + t;
@@ -1168,7 +1338,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // residual pieces of slab I+1 are requested before slab I's stores: loads
     // and stores share one in-order counter, so a load issued after a store
     // could only be waited for together with that store.
-    auto finish_slab_sig = [&](auto I_, u32x4 (&cur)[4], u32x4 (&nxt)[4]) {
+    auto finish_slab_sig = [&](auto I_, u32x4 (&cur)[4], u32x4 (&nxt)[4]) __attribute__((always_inline)) {
       constexpr int I = decltype(I_)::value;
       __builtin_amdgcn_s_waitcnt(0xc07f);
       __builtin_amdgcn_wave_barrier();
@@ -1191,20 +1361,124 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       gap_from_acc<T, NJ, SIG == kSigConvBiasReluGap>(a, acc, m0, n0, rowbase, colbase, wn, lr, lh,
                                                        pre_ch, rbias, red,
                                                        subt ? (rowbase < SR ? 1 : 0) : 4);
+    } else if (PIPE == 3 && m0 + BM <= a.M && n0 + BN <= a.N && vec_ok) {
+      // Four-wave form, whole tile: the 8 passes (32-row slab I, 64-column
+      // half H) alternate between the wave's two slabs, the next pass staged
+      // before the current one is read back (LDS operations of a wave run in
+      // order, so only the compiler's ordering needs a fence); a lane
+      // finishes rows rowbase + I*32 + rg*4 + t of columns colbase + H*64 +
+      // q*8 .. +7.  No row or column bounds, 32-bit offsets stepping by rows,
+      // one 16-byte store per row; residual pieces are requested two passes
+      // ahead.
+      if constexpr (PIPE == 3) {
+        const float alpha = a.alpha;
+        const uint32_t ldc2 = (uint32_t)a.ldc * 2u;
+        const uint32_t base0 =
+            (uint32_t)((((int)m0 + rowbase + rg * 4) * (int)a.ldc + (int)n0 + colbase + q * 8) * 2);
+        float* slab1 = slab + 8 * kSlabU * 4;
+        float bc[2][8];
+        if constexpr (SIG == kSigBiasGeluTanhScale) {
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+            ld8<T>((const T*)a.epi.ptr[0] + n0 + colbase + h * 64 + q * 8, true, 8, bc[h]);
+        }
+        u32x4 res[3][4];
+        auto pass_off = [&](int P, int t) __attribute__((always_inline)) -> uint32_t {
+          return base0 + (uint32_t)((P >> 1) * 32 + t) * ldc2 + (uint32_t)(P & 1) * 128u;
+        };
+        auto load_res3 = [&](auto P_) __attribute__((always_inline)) {
+          constexpr int P = decltype(P_)::value;
+          if constexpr (SIG == kSigAdd && P < 8) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+              res[P % 3][t] = __builtin_bit_cast(
+                  u32x4, __builtin_amdgcn_raw_buffer_load_b128(rres, (int)pass_off(P, t), 0, 0));
+          }
+        };
+        auto stage3 = [&](auto P_) __attribute__((always_inline)) {
+          constexpr int P = decltype(P_)::value;
+          if constexpr (P < 8) {
+            float* sl = (P & 1) ? slab1 : slab;
+            if constexpr ((P & 1) == 0)
+              stage_slab<P / 2, NJ, 0>(acc, sl, lh, lr);
+            else
+              stage_slab<P / 2, NJ, 2>(acc, sl, lh, lr);
+          }
+          __builtin_amdgcn_wave_barrier();
+        };
+        auto pass3 = [&](auto P_) __attribute__((always_inline)) {
+          constexpr int P = decltype(P_)::value;
+          stage3(std::integral_constant<int, P + 1>{});
+          load_res3(std::integral_constant<int, P + 2>{});
+          const float* sl = (P & 1) ? slab1 : slab;
+          f32x4 u[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) u[k] = *(const f32x4*)(sl + (rg * kSlabU + q * 8 + k) * 4);
+          __builtin_amdgcn_wave_barrier();
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            float v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float x = u[e][t];
+              if constexpr (SIG == kSigBiasGeluTanhScale)
+                v[e] = gelu_tanh(fmaf(x, alpha, bc[P & 1][e])) * a.epi.s[2];
+              else if constexpr (SIG == kSigGeluErf)
+                v[e] = gelu_erf_bf16out(x * alpha);
+              else
+                v[e] = x * alpha;
+            }
+            if constexpr (SIG == kSigAdd) {
+              const u32x4 r = res[P % 3][t];
+#pragma unroll
+              for (int k = 0; k < 4; ++k) {
+                v[2 * k] += __uint_as_float(r[k] << 16);
+                v[2 * k + 1] += __uint_as_float(r[k] & 0xFFFF0000u);
+              }
+            }
+            u32x4 o;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) o[k] = pack2_bf16(v[2 * k], v[2 * k + 1]);
+            __builtin_amdgcn_raw_buffer_store_b128(o, rcst, (int)pass_off(P, t), 0, 0);
+          }
+        };
+        stage3(std::integral_constant<int, 0>{});
+        load_res3(std::integral_constant<int, 0>{});
+        load_res3(std::integral_constant<int, 1>{});
+        pass3(std::integral_constant<int, 0>{});
+        pass3(std::integral_constant<int, 1>{});
+        pass3(std::integral_constant<int, 2>{});
+        pass3(std::integral_constant<int, 3>{});
+        pass3(std::integral_constant<int, 4>{});
+        pass3(std::integral_constant<int, 5>{});
+        pass3(std::integral_constant<int, 6>{});
+        pass3(std::integral_constant<int, 7>{});
+      }
     } else if constexpr (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
                          SIG == kSigBiasGeluTanhScale) {
       // (The softmax-partial chain keeps the rolled loop: unrolled, its
       // live values spill.)
-      u32x4 ra[4], rb[4];
-      if constexpr (SIG == kSigAdd) load_res(0, ra);
-      stage_slab<0, NJ>(acc, slab, lh, lr);
-      finish_slab_sig(std::integral_constant<int, 0>{}, ra, rb);
-      stage_slab<1, NJ>(acc, slab, lh, lr);
-      finish_slab_sig(std::integral_constant<int, 1>{}, rb, ra);
-      stage_slab<2, NJ>(acc, slab, lh, lr);
-      finish_slab_sig(std::integral_constant<int, 2>{}, ra, rb);
-      stage_slab<3, NJ>(acc, slab, lh, lr);
-      finish_slab_sig(std::integral_constant<int, 3>{}, rb, ra);
+      auto half = [&](auto H_) __attribute__((always_inline)) {
+        constexpr int H = decltype(H_)::value;
+        if constexpr (H > 0) {
+          col0 = n0 + colbase + H * 64 + q * 8;
+          valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
+          if constexpr (SIG == kSigBiasGeluTanhScale)
+            ld8<T>((const T*)a.epi.ptr[0] + col0, valid == 8 && vec_ok, valid, bcol);
+        }
+        u32x4 ra[4], rb[4];
+        if constexpr (SIG == kSigAdd) load_res(0, ra);
+        stage_slab<0, NJ, 2 * H>(acc, slab, lh, lr);
+        finish_slab_sig(std::integral_constant<int, 0>{}, ra, rb);
+        stage_slab<1, NJ, 2 * H>(acc, slab, lh, lr);
+        finish_slab_sig(std::integral_constant<int, 1>{}, rb, ra);
+        stage_slab<2, NJ, 2 * H>(acc, slab, lh, lr);
+        finish_slab_sig(std::integral_constant<int, 2>{}, ra, rb);
+        stage_slab<3, NJ, 2 * H>(acc, slab, lh, lr);
+        finish_slab_sig(std::integral_constant<int, 3>{}, rb, ra);
+      };
+      half(std::integral_constant<int, 0>{});
+      if constexpr (NJ == 4) half(std::integral_constant<int, 1>{});
     } else {
       // A switch keeps every acc index static while the finishing code
       // exists once (the loop itself is not unrolled).
@@ -1416,6 +1690,20 @@ static bool conv_wide(int dtype, const GemmArgs& a) {
                                            a.terminal == TERM_GAP, a.pool);
 }
 
+// The four-wave form (one wave per SIMD, 128 x 128 per wave) runs the
+// compiled chains without a terminal when K is a multiple of the 64-deep
+// stage.  MK_GEMM_WAVES=8 in the environment keeps the eight-wave form (for
+// side-by-side measurement).
+static bool four_wave_form(const GemmArgs& a, int sig) {
+  static const int forced = [] {
+    const char* e = getenv("MK_GEMM_WAVES");
+    return e ? atoi(e) : 0;
+  }();
+  if (forced == 8) return false;
+  return a.K % 64 == 0 && (sig == kSigNone || sig == kSigGeluErf || sig == kSigAdd ||
+                           sig == kSigBiasGeluTanhScale);
+}
+
 template <typename T>
 static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
   // Conv GEMMs: the bf16 (channel bias, ReLU, average pool) chain on the
@@ -1436,7 +1724,24 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
     hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 2, 0, 2, 128, kSigGeneric>), grid,
                        dim3(512), 0, st, a);
   } else {
-    switch (gemm_signature(a)) {
+    const int sig = gemm_signature(a);
+    if (four_wave_form(a, sig)) {
+      switch (sig) {
+#define MK_GEMM_SIG4(SIG)                                                                     \
+  case SIG:                                                                                   \
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kGemmTileN, 2, 0, 3, 128, SIG>), grid, dim3(256), \
+                       0, st, a);                                                             \
+    break;
+        MK_GEMM_SIG4(kSigNone)
+        MK_GEMM_SIG4(kSigGeluErf)
+        MK_GEMM_SIG4(kSigAdd)
+        default:
+          MK_GEMM_SIG4(kSigBiasGeluTanhScale)
+#undef MK_GEMM_SIG4
+      }
+      return;
+    }
+    switch (sig) {
 #define MK_GEMM_SIG(SIG)                                                                      \
   case SIG:                                                                                   \
     hipLaunchKernelGGL((gemm_mfma_kernel<T, 4, kGemmTileN, 2, 0, 2, 128, SIG>), grid, dim3(512), \

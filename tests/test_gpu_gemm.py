@@ -200,3 +200,21 @@ def test_gemm_big_tiles_f32(epi):
     module = gemm_module(2100, 2056, 72, 0, dtype="f32", epi=epi)
     rep, m, *_ = run_parity(module, [0] * (1 + len(epi)))
     assert rep["pass"], describe(rep)
+
+
+# K a multiple of the 64-deep stage: the compiled chains without a terminal
+# run on four waves of 128 x 128 each, the stage loop in groups of six; 1, 5,
+# 6 and 7 stages cover a lone stage, the remainder, one whole group and a group
+# plus one.  Ragged M and N, and N = 2053 for unaligned output rows.
+FOUR_WAVE_CHAINS = [(), ("GELU_ERF",), ("ADD",), ("BIAS", "GELU_TANH", "SCALE")]
+
+
+@pytest.mark.parametrize("epi", FOUR_WAVE_CHAINS, ids=lambda e: "+".join(e) or "none")
+@pytest.mark.parametrize("M,N,K", [(2100, 2056, 64), (2071, 2053, 320), (2048, 2048, 384),
+                                   (2100, 2056, 448)])
+def test_gemm_big_tiles_whole_stages(M, N, K, epi):
+    print(f"gemm big {M}x{N}x{K} {epi}", flush=True)
+    module = gemm_module(M, N, K, 0, epi=epi)
+    rep, m, out, *_ = run_parity(module, [0] * (1 + len(epi)))
+    assert m.subkernels()[0]["uses_mfma"]
+    assert rep["pass"], describe(rep)
