@@ -139,7 +139,8 @@ def causal_attention_block(B=2, S=256, D=512, H=4, dtype="bf16", x_std=1.0):
     w = (NORMAL, 0.0, 0.02)
     n = 3
     return {
-        "name": f"causal_attention_b{B}_s{S}_d{D}_h{H}_{dtype}",
+        "name": f"causal_attention_b{B}_s{S}_d{D}_h{H}" + (f"_x{x_std:g}" if x_std != 1.0 else "")
+                + f"_{dtype}",
         "dtype": dtype,
         "inputs": [[B, S, D], [3 * D, D], [D, D]],
         "recipes": [(NORMAL, 0.0, x_std), w, w],

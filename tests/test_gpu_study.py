@@ -7,6 +7,7 @@ sit exactly at the largest error seen), and the bugs that change the mutated
 stage far beyond rounding are caught by the decomposed check in every run,
 with a positive feasibility gap.  The full study (20 + 20 runs, larger
 blocks) is tests/verification_study.py."""
+import numpy as np
 import pytest
 import torch
 
@@ -34,9 +35,40 @@ def test_reduced_study():
     print(md)
     for key, b in res["blocks"].items():
         v = b["variants"]
+        if key.startswith("attention_large_scores"):
+            # scores beyond exp's range: the unsafe softmax makes NaN rows.
+            # (Its correct runs are not bounded here: scores near 100 carry
+            # bf16 ulps of 0.5 - 1 in the QK stage, so a 20-run max + 3 sigma
+            # tolerance is coarse and rejects some correct runs; the full
+            # study reports the count.)
+            assert v["Unsafe softmax"]["decomposed_caught"] == 10, key
+            assert v["Unsafe softmax"]["e2e_caught"]["0.1"] == 10, key
+            continue
         assert v["correct"]["decomposed_caught"] <= 2, key
         robust = ROBUST_F32 if key.endswith("_f32") else ROBUST
         for name, r in v.items():
             if name in robust:
                 assert r["decomposed_caught"] == 10, f"{key}: {name}"
                 assert r["gap_dec"] > 0, f"{key}: {name}"
+
+
+def test_reduced_error_profiles():
+    """App. D's error-profile tables at reduced size (3 runs, N up to 256):
+    every error finite; bf16 errors above fp32 errors for the contractions;
+    matmul errors growing with the input scale in both dtypes (the error of a
+    dot product scales with the product of the operand scales)."""
+    import error_profiles
+    print("reduced error profiles (3 runs)", flush=True)
+    res = error_profiles.run_all(runs=3, dims=[64, 256], quick=True,
+                                 log=lambda *a: print(*a, flush=True))
+    print(error_profiles.to_markdown(res))
+    for name, r in res["profiles"].items():
+        for dt in ("f32", "bf16"):
+            assert all(np.isfinite(r[dt]["max"])), name
+    for name in ("Matmul 512^2", "Conv2d 8x64x32x32 -> 64, 3x3"):
+        r = res["profiles"][name]
+        assert max(r["f32"]["max"]) < 1e-2 and max(r["f32"]["max"]) < min(r["bf16"]["max"]), name
+    d = res["input_dependence"]
+    for dt in ("f32", "bf16"):
+        a, b, c = (max(d[k][dt]["max"]) for k in ("N(0, 0.01^2)", "N(0, 1)", "N(0, 10^2)"))
+        assert a < b < c, (dt, a, b, c)
