@@ -105,7 +105,7 @@ __device__ __forceinline__ float epi_apply(const EpiDev& e, float v, int64_t row
       case EPI_BIAS_COL: v += ld<T>((const T*)e.ptr[i], col); break;
       case EPI_BIAS_CH: v += ld<T>((const T*)e.ptr[i], ch); break;
       case EPI_RELU: v = fmaxf(v, 0.0f); break;
-      case EPI_GELU_ERF: v = gelu_erf(v); break;
+      case EPI_GELU_ERF: v = sizeof(T) == 2 ? gelu_erf_bf16out(v) : gelu_erf(v); break;
       case EPI_GELU_TANH: v = gelu_tanh(v); break;
       case EPI_SCALE: v *= e.s[i]; break;
       case EPI_ADD: v += ld<T>((const T*)e.ptr[i], flat); break;
@@ -193,9 +193,10 @@ __device__ __forceinline__ void epi_apply8(const EpiDev& e, float (&v)[8], int64
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] = fmaxf(v[k], 0.0f);
         break;
-      case EPI_GELU_ERF:
+      case EPI_GELU_ERF:   // (the logistic form where the result is stored as bf16)
 #pragma unroll
-        for (int k = 0; k < 8; ++k) v[k] = gelu_erf(v[k]);
+        for (int k = 0; k < 8; ++k)
+          v[k] = sizeof(T) == 2 ? gelu_erf_bf16out(v[k]) : gelu_erf(v[k]);
         break;
       case EPI_GELU_TANH:
 #pragma unroll
