@@ -248,8 +248,8 @@ def main():
     t0 = time.perf_counter()
     host = inputs.make_inputs(module, args.seed)
     log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
-    fused = mk.Module(module, args.decomp)
-    split = None if args.no_split else mk.Module(module, "split")
+    fused = mk.Module(module, args.decomp, strict=True)
+    split = None if args.no_split else mk.Module(module, "split", strict=True)
     ws_bytes = max(fused.workspace_size(), split.workspace_size() if split else 0)
     ins, _, ws = mk.device_buffers(module, host, ws_bytes)
     out = mk.out_tensor(module, fused.info["out_shape"])

@@ -115,6 +115,23 @@ typedef enum {
 /* Implementation ids accepted by mk_subkernel_select. */
 enum { MK_IMPL_TUNED = 0, MK_IMPL_SIMPLE = 1, MK_IMPL_MUTANT_BASE = 100 };
 
+/* Why MK_IMPL_TUNED of a GEMM, CONV or ATTN subkernel runs the simple kernels
+ * (the ones MK_IMPL_SIMPLE selects) instead of the matrix-core kernels.  The
+ * results stay correct either way; mk_subkernel_info reports the code so a
+ * caller can tell, and the Python binding warns (or raises, strict=True). */
+typedef enum {
+  MK_LIMIT_NONE = 0,   /* the tuned kernels run (always for EW and ROW subkernels) */
+  MK_LIMIT_DTYPE = 1,  /* no matrix-core form for the dtype (fused attention: bf16 only) */
+  MK_LIMIT_ALIGN = 2,  /* K, a [K,N] weight's N, a leading dimension or a batch offset
+                          is not a multiple of 16 bytes (8 bf16 / 4 fp32 elements) */
+  MK_LIMIT_SHAPE = 3,  /* conv: C not a multiple of 32 (bf16) / 16 (fp32) channels,
+                          P*Q not a multiple of 8, or a pooled image smaller than a
+                          column tile; attention: head dim not 64 or 128; a row
+                          terminal (ROWSUM / SOFTMAX / LAYERNORM) after a batched GEMM */
+  MK_LIMIT_RANGE = 4   /* an operand slice of 2 GiB or more, or a grid past the launch
+                          limits */
+} mk_tuned_limit;
+
 typedef struct {
   int32_t n_subkernels;
   int32_t n_ops;
@@ -138,6 +155,8 @@ typedef struct {
   int32_t n_launches;             /* kernel launches of the selected implementation */
   int64_t scratch_bytes;          /* scratch the selected implementation uses */
   int32_t uses_mfma;              /* 1: the contraction runs on the matrix cores */
+  int32_t tuned_limit;            /* mk_tuned_limit of MK_IMPL_TUNED on this subkernel,
+                                     whichever impl is selected */
 } mk_subkernel_info_t;
 
 /* Fill group_of_op[n_ops] with a preset decomposition.  The groupings follow

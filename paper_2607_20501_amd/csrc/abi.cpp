@@ -124,6 +124,7 @@ mk_status mk_subkernel_info(const mk_module* m, int32_t i, mk_subkernel_info_t* 
   info->n_launches = mk::impl_launches(p, s, s.impl);
   info->scratch_bytes = mk::impl_scratch(p, s, s.impl);
   info->uses_mfma = mk::impl_uses_mfma(p, s, s.impl) ? 1 : 0;
+  info->tuned_limit = mk::tuned_limit(p, s);
   return MK_OK;
 }
 

@@ -177,6 +177,18 @@ bool impl_uses_mfma(const Plan& p, const Subkernel& sk, int impl) {
   return false;
 }
 
+int tuned_limit(const Plan& p, const Subkernel& sk) {
+  if (sk.family == MK_FAM_GEMM) return gemm_mfma_limit(p.dtype, gemm_probe(sk));
+  if (sk.family == MK_FAM_CONV) return conv_mfma_limit(p.dtype, conv_args(sk.conv));
+  if (sk.family == MK_FAM_ATTN) {
+    AttnArgs a{};
+    a.B = sk.attn.B; a.H = sk.attn.H; a.dh = sk.attn.dh; a.S = sk.attn.S;
+    a.causal = sk.attn.causal ? 1 : 0;
+    return attn_fused_limit(p.dtype, a);
+  }
+  return MK_LIMIT_NONE;
+}
+
 int impl_launches(const Plan& p, const Subkernel& sk, int impl) {
   if (sk.family == MK_FAM_GEMM) {
     const bool transpose = use_mfma(p, sk, impl) && sk.gemm.layout == 1;

@@ -18,6 +18,8 @@ int64_t impl_scratch(const Plan& p, const Subkernel& sk, int impl);
 int64_t max_scratch_bytes(const Plan& p, const Subkernel& sk);
 // Whether the implementation runs its contraction on the matrix cores.
 bool impl_uses_mfma(const Plan& p, const Subkernel& sk, int impl);
+// mk_tuned_limit of the tuned implementation on this subkernel.
+int tuned_limit(const Plan& p, const Subkernel& sk);
 
 // Optional launch-level timing: brackets each kernel launch with a pair of
 // HIP events taken from a pre-created pool (no synchronisation).

@@ -306,10 +306,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
 
 }  // namespace
 
-bool attn_fused_supported(int dtype, const AttnArgs& a) {
-  if (dtype != MK_BF16 || (a.dh != 64 && a.dh != 128)) return false;
+int attn_fused_limit(int dtype, const AttnArgs& a) {
+  if (dtype != MK_BF16) return MK_LIMIT_DTYPE;
+  if (a.dh != 64 && a.dh != 128) return MK_LIMIT_SHAPE;
   const int64_t ld3 = 3 * a.H * a.dh;
-  return a.S * ld3 * 2 < ((int64_t)1 << 31) && a.B * a.H * ((a.S + BQ - 1) / BQ) < (1ll << 31);
+  return a.S * ld3 * 2 < ((int64_t)1 << 31) && a.B * a.H * ((a.S + BQ - 1) / BQ) < (1ll << 31)
+             ? MK_LIMIT_NONE
+             : MK_LIMIT_RANGE;
+}
+
+bool attn_fused_supported(int dtype, const AttnArgs& a) {
+  return attn_fused_limit(dtype, a) == MK_LIMIT_NONE;
 }
 
 hipError_t launch_attn_fused(int dtype, const AttnArgs& a, hipStream_t st) {

@@ -233,17 +233,23 @@ __global__ void gap_finish_kernel(const float* partial, int64_t N, int64_t K, in
 
 static int64_t esize(int dtype) { return dtype == MK_BF16 ? 2 : 4; }
 
-bool conv_mfma_supported(int dtype, const ConvArgs& a) {
-  if (dtype != MK_BF16 && dtype != MK_F32) return false;
+int conv_mfma_limit(int dtype, const ConvArgs& a) {
+  if (dtype != MK_BF16 && dtype != MK_F32) return MK_LIMIT_DTYPE;
   // A K slice (32 bf16 / 16 fp32 channels of one (r, s)) must not cross an
   // (r, s) boundary; 8 consecutive positions stay in one image.
   const int64_t bk = dtype == MK_BF16 ? 32 : 16;
-  if (a.C % bk || (a.P * a.Q) % 8) return false;
+  if (a.C % bk || (a.P * a.Q) % 8) return MK_LIMIT_SHAPE;
   // a tile spans at most two images
   if (a.gap && a.P * a.Q < conv_gemm_tile_n(dtype, a.C, a.P * a.Q, a.epi, a.gap, a.pool))
-    return false;
+    return MK_LIMIT_SHAPE;
   const int64_t xp = a.N * (a.H + 2 * a.pad) * (a.W + 2 * a.pad) * a.C * esize(dtype);
-  return xp < ((int64_t)1 << 31) && a.K * a.R * a.S * a.C * esize(dtype) < ((int64_t)1 << 31);
+  return xp < ((int64_t)1 << 31) && a.K * a.R * a.S * a.C * esize(dtype) < ((int64_t)1 << 31)
+             ? MK_LIMIT_NONE
+             : MK_LIMIT_RANGE;
+}
+
+bool conv_mfma_supported(int dtype, const ConvArgs& a) {
+  return conv_mfma_limit(dtype, a) == MK_LIMIT_NONE;
 }
 
 ConvScratch conv_mfma_scratch(int dtype, const ConvArgs& a) {

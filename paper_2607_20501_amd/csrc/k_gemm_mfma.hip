@@ -1586,23 +1586,29 @@ __global__ __launch_bounds__(256) void transpose_b_kernel(GemmArgs a, T* dst) {
 
 }  // namespace
 
-bool gemm_mfma_supported(int dtype, const GemmArgs& a) {
-  if (dtype != MK_BF16 && dtype != MK_F32) return false;
+int gemm_mfma_limit(int dtype, const GemmArgs& a) {
+  if (dtype != MK_BF16 && dtype != MK_F32) return MK_LIMIT_DTYPE;
   const int64_t es = dtype == MK_BF16 ? 2 : 4, E = 16 / es;
+  if (a.M < 1 || a.N < 1 || a.K < 1) return MK_LIMIT_SHAPE;
   // 16-byte operand chunks: K (and N for a [K, N] weight), leading dimensions
   // and batch offsets must be multiples of the chunk.
-  if (a.K % E || a.lda % E || a.ldb % E) return false;
-  if (a.layout == 1 && a.N % E) return false;
+  if (a.K % E || a.lda % E || a.ldb % E) return MK_LIMIT_ALIGN;
+  if (a.layout == 1 && a.N % E) return MK_LIMIT_ALIGN;
   const int64_t offs[] = {a.a_off, a.a_sb, a.a_sh, a.b_off, a.b_sb, a.b_sh};
   for (int64_t o : offs)
-    if (o % E) return false;
-  if (a.M < 1 || a.N < 1 || a.K < 1) return false;
-  if (a.terminal != TERM_NONE && a.batch * a.heads != 1) return false;
+    if (o % E) return MK_LIMIT_ALIGN;
+  // a row terminal (ROWSUM / SOFTMAX / LAYERNORM) is finished over one matrix
+  if (a.terminal != TERM_NONE && a.batch * a.heads != 1) return MK_LIMIT_SHAPE;
   // Buffer-resource ranges are 32-bit: every operand slice must stay below 2 GB.
   const int64_t lim = (int64_t)1 << 31;
-  if (a.M * a.lda * es >= lim || a.N * (a.layout == 0 ? a.ldb : a.K) * es >= lim) return false;
+  if (a.M * a.lda * es >= lim || a.N * (a.layout == 0 ? a.ldb : a.K) * es >= lim)
+    return MK_LIMIT_RANGE;
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + 127) / 128);
-  return tiles < (1ll << 31) && a.batch * a.heads <= 65535;
+  return tiles < (1ll << 31) && a.batch * a.heads <= 65535 ? MK_LIMIT_NONE : MK_LIMIT_RANGE;
+}
+
+bool gemm_mfma_supported(int dtype, const GemmArgs& a) {
+  return gemm_mfma_limit(dtype, a) == MK_LIMIT_NONE;
 }
 
 int64_t gemm_mfma_bt_bytes(int dtype, const GemmArgs& a) {

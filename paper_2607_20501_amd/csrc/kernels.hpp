@@ -133,6 +133,9 @@ bool conv_bias_relu_gap_wide(int dtype, int64_t C, int64_t PQ, const EpiDev& epi
                              int pool);
 int64_t conv_gemm_tile_n(int dtype, int64_t C, int64_t PQ, const EpiDev& epi, bool gap,
                          int pool);
+// mk_tuned_limit code: why these arguments cannot run on the MFMA kernel
+// (MK_LIMIT_NONE when they can).
+int gemm_mfma_limit(int dtype, const GemmArgs& a);
 bool gemm_mfma_supported(int dtype, const GemmArgs& a);   // bf16 or fp32
 // The MFMA kernel takes B as [N, K]; a [K, N] operand (layout 1) is first
 // transposed into scratch of gemm_mfma_bt_bytes() bytes, and gemm_with_bt()
@@ -154,11 +157,13 @@ hipError_t launch_gemm_small(int dtype, const GemmArgs& a, hipStream_t st);
 struct ConvScratch {
   int64_t xp_bytes, wp_bytes, partial_bytes;
 };
+int conv_mfma_limit(int dtype, const ConvArgs& a);
 bool conv_mfma_supported(int dtype, const ConvArgs& a);
 ConvScratch conv_mfma_scratch(int dtype, const ConvArgs& a);
 hipError_t launch_conv_pack(int dtype, const ConvArgs& a, void* xp, void* wp, hipStream_t st);
 GemmArgs conv_gemm_args(const ConvArgs& a, const void* xp, const void* wp, float* partial);
 hipError_t launch_gap_finish(int dtype, const ConvArgs& a, const float* partial, hipStream_t st);
+int attn_fused_limit(int dtype, const AttnArgs& a);
 bool attn_fused_supported(int dtype, const AttnArgs& a);
 hipError_t launch_attn_fused(int dtype, const AttnArgs& a, hipStream_t st);
 

@@ -6,6 +6,7 @@ PyTorch provides device memory and streams.  The functions keep the C names;
 """
 import ctypes
 import os
+import warnings
 
 import numpy as np
 
@@ -18,6 +19,9 @@ KINDS = ["GEMM", "BIAS", "BIAS_CHANNEL", "RELU", "GELU_ERF", "GELU_TANH", "SCALE
          "ROWSUM", "SOFTMAX", "LAYERNORM", "CONV2D", "GAP", "QK", "CAUSAL_MASK", "PV",
          "GMP", "LPPOOL"]
 FAMILIES = ["GEMM", "CONV", "EW", "ROW", "ATTN"]
+# mk_tuned_limit: why the tuned implementation of a contraction subkernel
+# runs the simple kernels ("none": it does not).
+TUNED_LIMITS = ["none", "dtype", "align", "shape", "range"]
 STATUS = ["MK_OK", "MK_E_INVALID_ARG", "MK_E_SHAPE", "MK_E_DTYPE", "MK_E_DECOMP",
           "MK_E_UNSUPPORTED", "MK_E_WORKSPACE", "MK_E_HIP", "MK_E_INTERNAL"]
 IMPL_TUNED, IMPL_SIMPLE = 0, 1
@@ -28,6 +32,11 @@ class MkError(RuntimeError):
     def __init__(self, status, msg):
         super().__init__(f"{STATUS[status] if 0 <= status < len(STATUS) else status}: {msg}")
         self.status = status
+
+
+class TunedLimitWarning(UserWarning):
+    """The tuned implementation of a subkernel runs the simple kernels on
+    these shapes (mk_tuned_limit); results are unaffected, speed is not."""
 
 
 class mk_shape(ctypes.Structure):
@@ -59,7 +68,7 @@ class mk_subkernel_info_t(ctypes.Structure):
                 ("flops", ctypes.c_int64), ("alg_bytes", ctypes.c_int64),
                 ("family", ctypes.c_int32), ("impl", ctypes.c_int32),
                 ("n_launches", ctypes.c_int32), ("scratch_bytes", ctypes.c_int64),
-                ("uses_mfma", ctypes.c_int32)]
+                ("uses_mfma", ctypes.c_int32), ("tuned_limit", ctypes.c_int32)]
 
 
 class mk_check(ctypes.Structure):
@@ -217,7 +226,8 @@ def mk_subkernel_info(h, i):
             "out_shape": _shape(s.out_shape), "out_bytes": s.out_bytes,
             "ws_offset": s.ws_offset, "flops": s.flops, "alg_bytes": s.alg_bytes,
             "family": FAMILIES[s.family], "impl": s.impl, "n_launches": s.n_launches,
-            "scratch_bytes": s.scratch_bytes, "uses_mfma": bool(s.uses_mfma)}
+            "scratch_bytes": s.scratch_bytes, "uses_mfma": bool(s.uses_mfma),
+            "tuned_limit": TUNED_LIMITS[s.tuned_limit]}
 
 
 def mk_subkernel_select(h, i, impl):
@@ -329,7 +339,9 @@ def mk_budget_shares(ms, needs_work=None):
 class Module:
     """A created module plus its device buffers (torch tensors)."""
 
-    def __init__(self, module, groups):
+    def __init__(self, module, groups, strict=False):
+        """strict: raise instead of warning when the tuned implementation of
+        a subkernel cannot use its matrix-core kernels on these shapes."""
         if isinstance(groups, str):
             groups = mk_decomposition_preset(module, groups)
         self.desc = module
@@ -337,6 +349,15 @@ class Module:
         self.h = mk_module_create(module, self.groups)
         self.info = mk_module_info(self.h)
         self.n = self.info["n_subkernels"]
+        limited = [(i, s["family"], s["tuned_limit"]) for i, s in enumerate(self.subkernels())
+                   if s["tuned_limit"] != "none"]
+        if limited:
+            msg = (f"module {module.get('name', '?')}: the tuned implementation runs the simple "
+                   "kernels for " + ", ".join(f"subkernel {i} ({f}, limit '{lim}')"
+                                              for i, f, lim in limited))
+            if strict:
+                raise MkError(STATUS.index("MK_E_UNSUPPORTED"), msg)
+            warnings.warn(msg, TunedLimitWarning, stacklevel=2)
 
     def __del__(self):
         h = getattr(self, "h", None)

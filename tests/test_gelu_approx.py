@@ -26,9 +26,9 @@ def _constants():
 def _gelu_fp32(x):
     cap, k0, k1, k2 = _constants()
     x = x.astype(np.float32)
-    x2 = np.minimum(x * x, np.float32(cap))
-    p = (k2 * x2 + k1) * x2 + k0
-    with np.errstate(over="ignore"):
+    with np.errstate(over="ignore"):   # x * x may overflow to inf; the cap takes it
+        x2 = np.minimum(x * x, np.float32(cap))
+        p = (k2 * x2 + k1) * x2 + k0
         e = np.exp2(x * p).astype(np.float32)
         return x * (np.float32(1) / (np.float32(1) + e))
 

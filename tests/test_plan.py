@@ -237,3 +237,48 @@ def test_empty_dimensions_are_rejected_by_both_sides():
     m = workloads.conv_relu_gap(N=1, C=4, H=0, W=5, K=3)
     with pytest.raises(mk.MkError):
         mk.mk_module_create(m, [0, 0, 0, 0])
+
+
+def test_tuned_limit_is_reported_and_strict_mode_raises():
+    """The tuned implementation names why it runs the simple kernels
+    (mk_tuned_limit), the binding warns about it, and strict=True refuses."""
+    cases = [
+        (workloads.linear_relu_rowsum(M=64, K=256, N=128, dtype="bf16"), [0, 0, 0, 0],
+         {0: "none"}),
+        (workloads.linear_relu_rowsum(M=64, K=250, N=128, dtype="bf16"), [0, 0, 0, 0],
+         {0: "align"}),   # K not a multiple of 8 bf16
+        (workloads.linear_relu_rowsum(M=64, K=126, N=128, dtype="f32"), [0, 0, 0, 0],
+         {0: "align"}),   # K not a multiple of 4 fp32
+        (workloads.gemm_gelu_softmax(M=64, K=64, N=100, dtype="bf16"), [0, 0, 0, 0, 0],
+         {0: "align"}),   # [K, N] weight with N not a multiple of 8
+        (workloads.conv_relu_gap(N=2, C=5, H=9, W=7, K=6), [0, 0, 0, 0], {0: "shape"}),
+        (workloads.conv_relu_gap(N=2, C=64, H=16, W=16, K=32), [0, 0, 0, 0], {0: "none"}),
+        (workloads.conv_relu_gap(N=2, C=64, H=8, W=8, K=32), [0, 0, 0, 0],
+         {0: "shape"}),   # pooled 8 x 8 image smaller than a column tile
+        (workloads.causal_attention_block(B=1, S=64, D=128, H=2, dtype="bf16"),
+         [0, 1, 1, 1, 1, 2], {0: "none", 1: "none", 2: "none"}),
+        (workloads.causal_attention_block(B=1, S=64, D=128, H=2, dtype="f32"),
+         [0, 1, 1, 1, 1, 2], {0: "none", 1: "dtype", 2: "none"}),
+        (workloads.causal_attention_block(B=1, S=64, D=128, H=4, dtype="bf16"),
+         [0, 1, 1, 1, 1, 2], {0: "none", 1: "shape", 2: "none"}),   # head dim 32
+    ]
+    for module, groups, want in cases:
+        with __import__("warnings").catch_warnings(record=True) as w:
+            __import__("warnings").simplefilter("always")
+            m = mk.Module(module, groups)
+        got = {i: s["tuned_limit"] for i, s in enumerate(m.subkernels())}
+        assert got == want, module["name"]
+        limited = any(v != "none" for v in want.values())
+        assert any(issubclass(x.category, mk.TunedLimitWarning) for x in w) == limited
+        if limited:
+            with pytest.raises(mk.MkError) as e:
+                mk.Module(module, groups, strict=True)
+            assert e.value.status == 5          # MK_E_UNSUPPORTED
+        else:
+            mk.Module(module, groups, strict=True)
+        m.select(0, mk.IMPL_SIMPLE)               # reported whichever impl is selected
+        assert m.subkernels()[0]["tuned_limit"] == want[0]
+    for k in range(1, 6):                         # every full-size workload runs tuned
+        full = workloads.full_size(k)
+        for preset in ("split", "fused"):
+            mk.Module(full, preset, strict=True)
