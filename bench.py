@@ -10,8 +10,9 @@ selects the others.
 
 Prints ONE JSON line with the throughput of the fused composition (TFLOP/s of
 the module's algorithmic flops), the split composition beside it, the
-roofline of the dominant kernel (from HIP events around each launch, recorded
-live over the timed steps) and the oracle's CPU throughput on a bounded
+roofline of the dominant kernel (from a HIP event pair around that launch,
+recorded over as many runs as the timed steps, the other launches back to
+back) and the oracle's CPU throughput on a bounded
 sample of independent units -- rows, images or sequences -- which also checks
 those units of the GPU output).
 """
@@ -105,10 +106,11 @@ def measured_traffic(workload, kernel):
 
 def time_module(mod, ins, out, ws, steps, warmup):
     """ms per step over `steps` back-to-back runs (after `warmup` untimed
-    ones), bracketed by device synchronisation; then the same number of runs
-    again with a HIP event pair around every launch (on the module's stream)
-    for per-launch durations.  The event records add a few microseconds per
-    launch, so they stay out of the timed region."""
+    ones), bracketed by device synchronisation; then, for each launch k of a
+    run, `steps` more runs with a HIP event pair around launch k alone (the
+    other launches run back to back, as in the timed steps) for per-launch
+    durations.  An event pair adds the launch's dispatch time (a few
+    microseconds) to its figure, so the pairs stay out of the timed region."""
     import torch
     for _ in range(warmup):
         mod.run(ins, out, ws)
@@ -120,13 +122,14 @@ def time_module(mod, ins, out, ws, steps, warmup):
     end.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / steps
-    per_run = mod.launches_per_run()
-    mod.profile_begin(per_run * steps)
-    for _ in range(steps):
-        mod.run(ins, out, ws)
-    torch.cuda.synchronize()
-    launch_ms = mod.profile_end(per_run * steps)
-    per_launch = [sum(launch_ms[k::per_run]) / steps for k in range(per_run)]
+    per_launch = []
+    for k in range(mod.launches_per_run()):
+        mod.profile_begin(steps, only_launch=k)
+        for _ in range(steps):
+            mod.run(ins, out, ws)
+        torch.cuda.synchronize()
+        launch_ms = mod.profile_end(steps)
+        per_launch.append(sum(launch_ms) / len(launch_ms))
     return ms, per_launch
 
 

@@ -234,15 +234,22 @@ mk_status mk_run_noalloc(mk_module* m, const void* const* dev_inputs, void* dev_
 
 /* Launch-level profiling (timing of each kernel launch, for roofline
  * figures; Sec. 4 times kernels with HIP / CUDA events over repeated runs
- * after warm-up).  While a profile is open, every mk_run of the module also brackets
- * each of its kernel launches with HIP events, without synchronising, until
- * max_launches launches are recorded (later launches are not recorded).
+ * after warm-up).  While a profile is open, every mk_run of the module also
+ * brackets its kernel launches with timing-only HIP events (no system-scope
+ * fence at each record), without synchronising, until max_launches launches
+ * are recorded (later launches are not recorded).  only_launch = -1 records
+ * every launch: a run contributes sum(mk_subkernel_info.n_launches)
+ * consecutive entries.  only_launch = k >= 0 records only the run's k-th
+ * launch (0-based, in launch order): one entry per run, the other launches
+ * run back to back without events, as in an unprofiled run (each event pair
+ * adds a few microseconds of dispatch time to the figure and an idle gap in
+ * the stream; a chip that runs at its power limit clocks higher after gaps).
  * mk_profile_end synchronises on the last recorded launch, writes the elapsed
  * milliseconds of the recorded launches in launch order to launch_ms (at most
- * capacity entries), sets *n_recorded and closes the profile.  A run
- * contributes sum(mk_subkernel_info.n_launches) consecutive entries.
- * MK_E_INVALID_ARG if a profile is already open / not open. */
-mk_status mk_profile_begin(mk_module* m, int32_t max_launches);
+ * capacity entries), sets *n_recorded and closes the profile.
+ * MK_E_INVALID_ARG if a profile is already open / not open, or only_launch is
+ * outside [-1, launches per run). */
+mk_status mk_profile_begin(mk_module* m, int32_t max_launches, int32_t only_launch);
 mk_status mk_profile_end(mk_module* m, float* launch_ms, int32_t capacity, int32_t* n_recorded);
 
 /* One reference check: stage s is subkernel s's materialised output (the last

@@ -202,6 +202,7 @@ mk_status mk_run(mk_module* m, const void* const* dev_inputs, void* dev_out, voi
       mk::LaunchTimer* tm = nullptr;
       if (m->profiling) {
         m->timer.stream = st;
+        if (i == 0) m->timer.pos = 0;
         tm = &m->timer;
       }
       s = mk::run_subkernel(p, sk, vals, vals[sk.out_value], scratch, st, tm);
@@ -317,13 +318,18 @@ mk_status mk_swap(mk_module* m, const void* const* dev_inputs, void* dev_out, vo
   }
 }
 
-mk_status mk_profile_begin(mk_module* m, int32_t max_launches) {
+mk_status mk_profile_begin(mk_module* m, int32_t max_launches, int32_t only_launch) {
   if (!m || max_launches < 1) return fail(MK_E_INVALID_ARG, "null module or max_launches < 1");
   if (m->profiling) return fail(MK_E_INVALID_ARG, "a profile is already open");
+  int32_t per_run = 0;
+  for (const mk::Subkernel& s : m->plan.subs) per_run += mk::impl_launches(m->plan, s, s.impl);
+  if (only_launch < -1 || only_launch >= per_run)
+    return fail(MK_E_INVALID_ARG, "only_launch out of range");
   for (hipEvent_t e : m->prof) (void)hipEventDestroy(e);
   m->prof.assign(2 * (size_t)max_launches, nullptr);
   for (auto& e : m->prof) {
-    hipError_t r = hipEventCreate(&e);
+    // timing only: no system-scope fence (cache write-back) at each record
+    hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
     if (r != hipSuccess) {
       e = nullptr;
       return hip_fail(r, "hipEventCreate");
@@ -331,6 +337,8 @@ mk_status mk_profile_begin(mk_module* m, int32_t max_launches) {
   }
   m->timer.events = &m->prof;
   m->timer.next = 0;
+  m->timer.only = only_launch;
+  m->timer.pos = 0;
   m->profiling = true;
   return MK_OK;
 }

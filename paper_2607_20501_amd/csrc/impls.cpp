@@ -237,11 +237,12 @@ static mk_status hip_check(hipError_t e, const char* what) {
 
 mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<void*>& vals,
                         void* out, void* scratch, hipStream_t st, LaunchTimer* tm) {
-  // Each launch is bracketed by tm->mark() when launch timing is active.
+  // Each launch is bracketed by tm->begin() / tm->end() when launch timing
+  // is active.
   auto timed = [tm](auto&& launch) {
-    if (tm) tm->mark();
+    if (tm) tm->begin();
     hipError_t e = launch();
-    if (tm) tm->mark();
+    if (tm) tm->end();
     return e;
   };
   const int impl = sk.impl;

@@ -24,11 +24,20 @@ int tuned_limit(const Plan& p, const Subkernel& sk);
 // Optional launch-level timing: brackets each kernel launch with a pair of
 // HIP events taken from a pre-created pool (no synchronisation).
 struct LaunchTimer {
-  std::vector<hipEvent_t>* events = nullptr;  // 2 per launch
+  std::vector<hipEvent_t>* events = nullptr;  // 2 per recorded launch
   size_t next = 0;                            // next free event
   hipStream_t stream = nullptr;
-  void mark() {
-    if (events && next < events->size()) (void)hipEventRecord((*events)[next++], stream);
+  int only = -1;      // >= 0: record only this launch index of each run
+  int pos = 0;        // launch index within the current run
+  bool on = false;    // the current launch is being recorded
+  void begin() {
+    const int idx = pos++;
+    on = events && next + 2 <= events->size() && (only < 0 || idx == only);
+    if (on) (void)hipEventRecord((*events)[next++], stream);
+  }
+  void end() {
+    if (on) (void)hipEventRecord((*events)[next++], stream);
+    on = false;
   }
 };
 

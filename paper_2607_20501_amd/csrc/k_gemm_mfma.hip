@@ -78,14 +78,21 @@ constexpr int kSigGeluErf = 3;           // exact GELU
 constexpr int kSigAdd = 4;               // residual add (operand laid out as C)
 constexpr int kSigBiasGeluTanhScaleSoftmax = 5;   // bias, tanh GELU, scale; softmax partials
 constexpr int kSigBiasGeluTanhScale = 6;          // bias, tanh GELU, scale
+constexpr int kSigBias = 7;                       // column bias
+
+// The compiled chains without a terminal (stored through a buffer resource).
+constexpr bool sig_plain(int sig) {
+  return sig == kSigNone || sig == kSigGeluErf || sig == kSigAdd || sig == kSigBiasGeluTanhScale ||
+         sig == kSigBias;
+}
+// Chains that start with a column bias (alpha * acc + bias as one FMA).
+constexpr bool sig_bias(int sig) {
+  return sig == kSigBiasGeluTanhScaleSoftmax || sig == kSigBiasGeluTanhScale || sig == kSigBias;
+}
 
 // Terminal of a signature (-1: read at run time).
 constexpr int sig_terminal(int sig) {
-  return sig == kSigBiasGeluTanhScaleSoftmax ? TERM_SOFTMAX
-         : (sig == kSigNone || sig == kSigGeluErf || sig == kSigAdd ||
-            sig == kSigBiasGeluTanhScale)
-             ? TERM_NONE
-             : -1;
+  return sig == kSigBiasGeluTanhScaleSoftmax ? TERM_SOFTMAX : sig_plain(sig) ? TERM_NONE : -1;
 }
 constexpr int kGroupM = 8;                        // tile rows per locality group
 constexpr int kXcds = 8;
@@ -624,8 +631,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   static_assert(WTN == 64 || (PIPE == 3 && WTN == 128),
                 "the epilogue maps 8 row groups x 8 column groups onto 64 columns of a wave");
   static_assert(PIPE != 3 || (!CONV && WN == 2 && BN == 256 && RB == 128 && sizeof(T) == 2 &&
-                              (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
-                               SIG == kSigBiasGeluTanhScale)),
+                              sig_plain(SIG)),
                 "the four-wave form runs plain bf16 GEMMs with a compiled chain, no terminal");
   constexpr int kRing = PIPE ? 5 * 32768 : kStages * kStageBytes;
   // (the four-wave epilogue alternates between two slabs per wave)
@@ -810,10 +816,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   };
   float bias_reg = load_bias_reg(it);
   bool staged0 = false;   // this tile's stage 0 was issued during the last epilogue
-  constexpr int kEpiVmem = (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
-                            SIG == kSigBiasGeluTanhScale)
-                               ? 16 * (NJ / 2)
-                               : 0;
+  constexpr int kEpiVmem = sig_plain(SIG) ? 16 * (NJ / 2) : 0;
   // Four-wave form: LDS byte offsets of the A slots (stage ks in ks % 3) and
   // B slots (ks % 2), and this lane's fragment address bases.  In a wave's
   // 128 x 128 tile, fragment (i, kk) of A reads row rowbase + i*32 + lr,
@@ -1144,8 +1147,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     const int64_t img = CONV ? (int64_t)((uint32_t)col0 / (uint32_t)PQ) : 0;   // positions < 2^31
 
     // Compiled TERM_NONE chains store through a buffer resource over C.
-    constexpr bool kBufStore = SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
-                               SIG == kSigBiasGeluTanhScale;
+    constexpr bool kBufStore = sig_plain(SIG);
     const __amdgpu_buffer_rsrc_t rcst =
         make_rsrc(C, kBufStore ? a.M * a.ldc * (int64_t)sizeof(T) : 0);
     // Residual operand (laid out as C; range checked by signature selection).
@@ -1154,7 +1156,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
                   SIG == kSigAdd ? a.M * a.ldc * (int64_t)sizeof(T) : 0);
     // Column bias of this lane's 8 columns, once per tile.
     float bcol[8];
-    if constexpr (SIG == kSigBiasGeluTanhScaleSoftmax || SIG == kSigBiasGeluTanhScale)
+    if constexpr (sig_bias(SIG))
       ld8<T>((const T*)a.epi.ptr[0] + col0, valid == 8 && vec_ok, valid, bcol);
 
     // One row of the lane: values v of columns col0 .. col0+7 of tile row
@@ -1190,6 +1192,9 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         const float sc = a.epi.s[2];
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = gelu_tanh(fmaf(v[e], a.alpha, bcol[e])) * sc;
+      } else if constexpr (SIG == kSigBias) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = fmaf(v[e], a.alpha, bcol[e]);
       } else if constexpr (SIG == kSigGeneric || SIG == kSigConvBiasReluGap) {
         if (a.epi.n && row_ok && valid > 0)
           epi_apply8<T>(a.epi, v, row, col0, row, valid, obase, valid == 8 && (CONV || vec_ok),
@@ -1353,7 +1358,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         float v[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          v[e] = SIG == kSigBiasGeluTanhScale ? u[e][t] : u[e][t] * a.alpha;
+          v[e] = SIG == kSigBiasGeluTanhScale || SIG == kSigBias ? u[e][t] : u[e][t] * a.alpha;
         finish_row(rowbase + I * 32 + rg * 4 + t, v, cur[t], 0.f);
       }
     };
@@ -1377,7 +1382,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
             (uint32_t)((((int)m0 + rowbase + rg * 4) * (int)a.ldc + (int)n0 + colbase + q * 8) * 2);
         float* slab1 = slab + 8 * kSlabU * 4;
         float bc[2][8];
-        if constexpr (SIG == kSigBiasGeluTanhScale) {
+        if constexpr (SIG == kSigBiasGeluTanhScale || SIG == kSigBias) {
 #pragma unroll
           for (int h = 0; h < 2; ++h)
             ld8<T>((const T*)a.epi.ptr[0] + n0 + colbase + h * 64 + q * 8, true, 8, bc[h]);
@@ -1423,6 +1428,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
               const float x = u[e][t];
               if constexpr (SIG == kSigBiasGeluTanhScale)
                 v[e] = gelu_tanh(fmaf(x, alpha, bc[P & 1][e])) * a.epi.s[2];
+              else if constexpr (SIG == kSigBias)
+                v[e] = fmaf(x, alpha, bc[P & 1][e]);
               else if constexpr (SIG == kSigGeluErf)
                 v[e] = gelu_erf_bf16out(x * alpha);
               else
@@ -1454,8 +1461,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         pass3(std::integral_constant<int, 6>{});
         pass3(std::integral_constant<int, 7>{});
       }
-    } else if constexpr (SIG == kSigNone || SIG == kSigGeluErf || SIG == kSigAdd ||
-                         SIG == kSigBiasGeluTanhScale) {
+    } else if constexpr (sig_plain(SIG)) {
       // (The softmax-partial chain keeps the rolled loop: unrolled, its
       // live values spill.)
       auto half = [&](auto H_) __attribute__((always_inline)) {
@@ -1463,7 +1469,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         if constexpr (H > 0) {
           col0 = n0 + colbase + H * 64 + q * 8;
           valid = (int)min<int64_t>(8, max<int64_t>(0, a.N - col0));
-          if constexpr (SIG == kSigBiasGeluTanhScale)
+          if constexpr (SIG == kSigBiasGeluTanhScale || SIG == kSigBias)
             ld8<T>((const T*)a.epi.ptr[0] + col0, valid == 8 && vec_ok, valid, bcol);
         }
         u32x4 ra[4], rb[4];
@@ -1658,15 +1664,17 @@ static int gemm_signature(const GemmArgs& a) {
   // (C and a residual are addressed through buffer resources: one batch,
   // 32-bit byte range)
   const bool buf = a.batch * a.heads == 1 && a.M * a.ldc * 2 < ((int64_t)1 << 31);
+  // (a column bias is read with 16-byte loads)
+  const bool bias_ok = e.n > 0 && e.code[0] == EPI_BIAS_COL && (uintptr_t)e.ptr[0] % 16 == 0;
   if (a.terminal == TERM_NONE && buf) {
     if (e.n == 0) return kSigNone;
     if (e.n == 1 && e.code[0] == EPI_GELU_ERF) return kSigGeluErf;
     if (e.n == 1 && e.code[0] == EPI_ADD) return kSigAdd;
-    if (e.n == 3 && e.code[0] == EPI_BIAS_COL && e.code[1] == EPI_GELU_TANH &&
-        e.code[2] == EPI_SCALE)
+    if (e.n == 1 && bias_ok) return kSigBias;
+    if (e.n == 3 && bias_ok && e.code[1] == EPI_GELU_TANH && e.code[2] == EPI_SCALE)
       return kSigBiasGeluTanhScale;
-  } else if (a.terminal == TERM_SOFTMAX && e.n == 3 && e.code[0] == EPI_BIAS_COL &&
-             e.code[1] == EPI_GELU_TANH && e.code[2] == EPI_SCALE) {
+  } else if (a.terminal == TERM_SOFTMAX && e.n == 3 && bias_ok && e.code[1] == EPI_GELU_TANH &&
+             e.code[2] == EPI_SCALE) {
     return kSigBiasGeluTanhScaleSoftmax;
   }
   return kSigGeneric;
@@ -1706,8 +1714,7 @@ static bool four_wave_form(const GemmArgs& a, int sig) {
     return e ? atoi(e) : 0;
   }();
   if (forced == 8) return false;
-  return a.K % 64 == 0 && (sig == kSigNone || sig == kSigGeluErf || sig == kSigAdd ||
-                           sig == kSigBiasGeluTanhScale);
+  return a.K % 64 == 0 && sig_plain(sig);
 }
 
 template <typename T>
@@ -1741,6 +1748,7 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
         MK_GEMM_SIG4(kSigNone)
         MK_GEMM_SIG4(kSigGeluErf)
         MK_GEMM_SIG4(kSigAdd)
+        MK_GEMM_SIG4(kSigBias)
         default:
           MK_GEMM_SIG4(kSigBiasGeluTanhScale)
 #undef MK_GEMM_SIG4
@@ -1758,6 +1766,7 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
       MK_GEMM_SIG(kSigAdd)
       MK_GEMM_SIG(kSigBiasGeluTanhScaleSoftmax)
       MK_GEMM_SIG(kSigBiasGeluTanhScale)
+      MK_GEMM_SIG(kSigBias)
       default:
         MK_GEMM_SIG(kSigGeneric)
 #undef MK_GEMM_SIG

@@ -135,7 +135,7 @@ def load():
               "mk_subkernel_info", "mk_subkernel_select", "mk_workspace_size", "mk_run",
               "mk_run_noalloc", "mk_verify"):
         getattr(lib, f).restype = ctypes.c_int
-    lib.mk_profile_begin.argtypes = [vp, ctypes.c_int32]
+    lib.mk_profile_begin.argtypes = [vp, ctypes.c_int32, ctypes.c_int32]
     lib.mk_profile_end.argtypes = [vp, P(ctypes.c_float), ctypes.c_int32, P(ctypes.c_int32)]
     lib.mk_profile_begin.restype = ctypes.c_int
     lib.mk_profile_end.restype = ctypes.c_int
@@ -255,8 +255,8 @@ def mk_run_noalloc(h, dev_inputs, dev_out, stream):
     _check(load().mk_run_noalloc(h, ptrs, dev_out, stream))
 
 
-def mk_profile_begin(h, max_launches):
-    _check(load().mk_profile_begin(h, int(max_launches)))
+def mk_profile_begin(h, max_launches, only_launch=-1):
+    _check(load().mk_profile_begin(h, int(max_launches), int(only_launch)))
 
 
 def mk_profile_end(h, capacity):
@@ -377,8 +377,8 @@ class Module:
     def launches_per_run(self):
         return sum(s["n_launches"] for s in self.subkernels())
 
-    def profile_begin(self, max_launches):
-        mk_profile_begin(self.h, max_launches)
+    def profile_begin(self, max_launches, only_launch=-1):
+        mk_profile_begin(self.h, max_launches, only_launch)
 
     def profile_end(self, capacity):
         return mk_profile_end(self.h, capacity)

@@ -175,10 +175,11 @@ def test_post_ln_ffn_block(shape, dec, dtype):
 
 # At least 64 tiles of 256 x 256 (smaller problems take the 64 x 64 kernel),
 # ragged in M and N; the chains compiled into their own epilogues (none, exact
-# GELU, residual add, bias + tanh GELU + scale + softmax partials) and the
+# GELU, residual add, column bias, bias + tanh GELU + scale + softmax
+# partials) and the
 # interpreted chain.  N = 2053 makes the output rows unaligned for 16-byte
 # stores (element-wise tail path).
-BIG_CHAINS = [(), ("GELU_ERF",), ("ADD",), ("BIAS", "GELU_TANH", "SCALE", "SOFTMAX"),
+BIG_CHAINS = [(), ("GELU_ERF",), ("ADD",), ("BIAS",), ("BIAS", "GELU_TANH", "SCALE", "SOFTMAX"),
               ("BIAS", "GELU_ERF", "SCALE", "ADD"), ("ROWSUM",)]
 
 
@@ -206,7 +207,7 @@ def test_gemm_big_tiles_f32(epi):
 # run on four waves of 128 x 128 each, the stage loop in groups of six; 1, 5,
 # 6 and 7 stages cover a lone stage, the remainder, one whole group and a group
 # plus one.  Ragged M and N, and N = 2053 for unaligned output rows.
-FOUR_WAVE_CHAINS = [(), ("GELU_ERF",), ("ADD",), ("BIAS", "GELU_TANH", "SCALE")]
+FOUR_WAVE_CHAINS = [(), ("GELU_ERF",), ("ADD",), ("BIAS",), ("BIAS", "GELU_TANH", "SCALE")]
 
 
 @pytest.mark.parametrize("epi", FOUR_WAVE_CHAINS, ids=lambda e: "+".join(e) or "none")

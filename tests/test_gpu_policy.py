@@ -38,3 +38,37 @@ def test_swap_applies_its_rule(make, dec, tau):
     assert rep["pass"], describe(rep)
     shares = mk.mk_budget_shares(r["ms_selected"])
     assert sum(shares) == pytest.approx(1.0, abs=1e-5)
+
+
+def test_launch_profile_every_launch_and_one_launch():
+    """mk_profile_begin / end: every launch of every run in launch order, the
+    max_launches cap, and one launch per run (the rest back to back)."""
+    module = workloads.gemm_gelu_softmax(M=1024, K=512, N=1024)
+    print(f"profile {module['name']}", flush=True)
+    m = mk.Module(module, "fused", strict=True)
+    host = inputs.make_inputs(module, 0)
+    ins, _, ws = mk.device_buffers(module, host, m.workspace_size())
+    out = mk.out_tensor(module, m.info["out_shape"])
+    per_run = m.launches_per_run()
+    assert per_run == 3                      # weight transpose, GEMM, softmax rows
+    runs = 6
+    m.run(ins, out, ws)
+    m.profile_begin(per_run * runs)
+    for _ in range(runs):
+        m.run(ins, out, ws)
+    every = m.profile_end(per_run * runs)
+    assert len(every) == per_run * runs and all(t > 0 for t in every)
+    m.profile_begin(4)                       # cap: later launches are not recorded
+    for _ in range(2):
+        m.run(ins, out, ws)
+    assert len(m.profile_end(16)) == 4
+    for k in range(per_run):
+        m.profile_begin(runs, only_launch=k)
+        for _ in range(runs):
+            m.run(ins, out, ws)
+        one = m.profile_end(runs)
+        assert len(one) == runs and all(t > 0 for t in one)
+        mean_every = sum(every[k::per_run]) / runs
+        assert 0.2 < (sum(one) / runs) / mean_every < 5, (k, one, every[k::per_run])
+    with pytest.raises(mk.MkError):
+        m.profile_begin(4, only_launch=per_run)

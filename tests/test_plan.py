@@ -282,3 +282,11 @@ def test_tuned_limit_is_reported_and_strict_mode_raises():
         full = workloads.full_size(k)
         for preset in ("split", "fused"):
             mk.Module(full, preset, strict=True)
+
+
+def test_profile_launch_index_is_checked_before_any_device_call():
+    m = mk.Module(workloads.gemm_gelu_softmax(M=64, K=64, N=512), "fused")
+    for bad in (-2, m.launches_per_run()):
+        with pytest.raises(mk.MkError) as e:
+            m.profile_begin(4, only_launch=bad)
+        assert e.value.status == 1            # MK_E_INVALID_ARG
