@@ -62,20 +62,42 @@ def test_mask_off_by_one_mutant_is_caught():
     assert rep["pass"], describe(rep)
 
 
-def test_fused_attention_growing_scores():
-    """Keys whose scale grows along the sequence (and a few large spikes), so
-    that the running maximum of a query's scores rises by many units after
-    the first key blocks: the fused kernel moves its softmax reference (and
-    rescales the partial output) only when the maximum exceeds it by more
-    than a fixed margin, and must still match the oracle."""
+def _scaled_key_bits(module, B, S, H, dh, ramp_to, spikes, seed=3):
+    """bf16 input bits with K scaled by a ramp 1 -> ramp_to along the keys and
+    by `spikes` ({key: factor}) at single keys."""
     from paper_2607_20501_amd import inputs
+    x = inputs.bf16_bits_to_f32(inputs.make_inputs(module, seed)[0]).reshape(B * S, 3 * H * dh)
+    key = np.arange(B * S) % S
+    ramp = (1.0 + (ramp_to - 1.0) * key / S).astype(np.float32)[:, None]
+    x[:, H * dh:2 * H * dh] *= ramp
+    for k, f in spikes.items():
+        x[k, H * dh:2 * H * dh] *= f
+    u = x.astype(np.float32).view(np.uint32)
+    return [((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16).ravel()]
+
+
+def test_fused_attention_growing_scores():
+    """Keys whose scale grows along the sequence, so that a query's scores
+    rise well above the maximum of its first key block (up to about 2^20 in
+    probability units): the fused kernel keeps the first block's maximum as
+    its softmax reference throughout (probabilities above 1 are held in fp32
+    / bf16) and must still match the oracle."""
     B, S, H, dh = 1, 1024, 2, 128
     module = attn_module(B, S, H, dh, True)
-    x = inputs.bf16_bits_to_f32(inputs.make_inputs(module, 3)[0]).reshape(B * S, 3 * H * dh)
-    key = np.arange(B * S) % S
-    ramp = (1.0 + 6.0 * key / S).astype(np.float32)[:, None]
-    x[:, H * dh:2 * H * dh] *= ramp                       # K grows along the keys
-    x[[100, 400, 700, 900], H * dh:2 * H * dh] *= 4.0     # and jumps at a few keys
-    bits = (x.astype(np.float32).view(np.uint32) + 0x7FFF + ((x.view(np.uint32) >> 16) & 1)) >> 16
-    rep, *_ = run_parity(module, [0] * len(module["ops"]), host=[bits.astype(np.uint16).ravel()])
+    host = _scaled_key_bits(module, B, S, H, dh, 3.0, {})
+    rep, *_ = run_parity(module, [0] * len(module["ops"]), host=host)
     assert rep["pass"], describe(rep)
+
+
+def test_fused_attention_overflow_path():
+    """Keys that grow far faster (and large spikes): some key blocks' scores
+    exceed the first block's maximum by more than 2^32 in probability units,
+    which the fixed-reference loop cannot hold; those waves recompute their
+    queries exactly on the kernel's slow path.  Every position must still
+    match the oracle, with and without a ragged tail."""
+    for B, S, H in [(1, 1024, 2), (2, 333, 1)]:
+        dh = 128
+        module = attn_module(B, S, H, dh, True)
+        host = _scaled_key_bits(module, B, S, H, dh, 7.0, {100 % S: 4.0, 400 % S: 6.0, 300: 8.0})
+        rep, *_ = run_parity(module, [0] * len(module["ops"]), host=host)
+        assert rep["pass"], describe(rep)
