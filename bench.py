@@ -71,7 +71,7 @@ def launch_names(mod):
                       "gemm_mfma_kernel (conv: " + ",".join(ops) + ")"]
             names += ["gap_finish_kernel"] * (n - 2)
         elif s["family"] == "ATTN":
-            names += ["attn_fwd_kernel (" + ",".join(ops) + ")"] * n
+            names += ["attn_fwd_pipe_kernel (" + ",".join(ops) + ")"] * n
         else:
             names += [s["family"].lower() + " subkernel (" + ",".join(ops) + ")"] * n
     return names

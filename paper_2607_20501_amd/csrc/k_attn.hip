@@ -63,11 +63,12 @@ __device__ __forceinline__ void wait_vm() {
 // O and Q in AGPRs), NW waves per workgroup sharing the K and V blocks.
 // Iteration j is software-pipelined:
 //   region 1: S(j+1) = K(j+1) Q^T on the matrix cores, one MFMA at a time,
-//             each followed by the exponentials of two scores of block j
-//             (and, spread over the slots, the loads of K(j+2) and V(j+1));
-//   region 2: O^T += V(j)^T P(j)^T, each MFMA followed by a part of the
-//             row sums of P(j); then (wave's last block only) the mask of
-//             S(j+1).
+//             each followed by the exponentials, packing and row sums of
+//             two of block j's probabilities;
+//   region 2: O^T += V(j)^T P(j)^T, each MFMA followed by the scaling of
+//             two of S(j+1)'s scores to log2 units relative to the
+//             reference (and, spread over the slots, the loads of K(j+2)
+//             and V(j+1)); then (wave's last block only) the mask of S(j+1).
 // K blocks and V blocks have two LDS slots each; a barrier at the top of
 // each iteration makes block j+1's K and block j's V visible to every wave
 // and frees the slots the iteration's loads overwrite.
@@ -166,7 +167,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
   constexpr int R2 = 4 * NDT * 2;           // MFMAs of region 2 (PV of a block)
   constexpr int EPS = 32 / R1;              // exp pairs per region-1 slot
   static_assert(LD * 16 * NT == KB, "block must split evenly over the threads");
-  static_assert(EPS * R1 == 32 && R2 % 8 == 0 && R1 % (2 * LD) == 0, "slot counts");
+  static_assert(EPS * R1 == 32 && 64 % R2 == 0 && R1 % (2 * LD) == 0, "slot counts");
   __shared__ __attribute__((aligned(1024))) char smem[4 * KB];   // K0 K1 V0 V1
 
   const int64_t S = a.S, H = a.H;
@@ -292,16 +293,21 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
   auto kfrag = [&](int slot, int ks, int kt) -> bf16x8 {
     return *(const bf16x8*)(smem + slot * KB + krd + kt * 32 * KROW + (((ks * 2 + lh) ^ kch) * 16));
   };
-  // Scores of pair e of 32 (qt = e/16, kt = e/8 % 2, registers 2(e%8), +1):
-  // s * scale * log2(e) - m, then (after exp2) packed into P.
-  auto fma_pair = [&](int C, int e, float (&d)[2]) {
+  // Pair e of 32 (qt = e/16, kt = e/8 % 2, registers 2(e%8), +1) of a block
+  // whose scores already hold s * scale * log2(e) - m: exp2, packed into P.
+  auto exp_pair = [&](int C, int e, float (&d)[2]) {
     const int qt = e >> 4, kt = (e >> 3) & 1, rp = e & 7;
-    d[0] = fmaf(sc[C][kt * 2 + qt][2 * rp], sl2, mneg[qt]);
-    d[1] = fmaf(sc[C][kt * 2 + qt][2 * rp + 1], sl2, mneg[qt]);
+    d[0] = __builtin_amdgcn_exp2f(sc[C][kt * 2 + qt][2 * rp]);
+    d[1] = __builtin_amdgcn_exp2f(sc[C][kt * 2 + qt][2 * rp + 1]);
   };
   auto pack_pair = [&](int e, const float (&d)[2]) {
     const int qt = e >> 4, kt = (e >> 3) & 1, rp = e & 7;
     pk[qt][kt * 2 + (rp >> 2)][rp & 3] = pack2_bf16(d[0], d[1]);
+  };
+  // Scores of tile m of block B_ to s * scale * log2(e) - m (registers r0 .. r0+n-1).
+  auto to_log2 = [&](int B_, int m, int r0, int n) {
+#pragma unroll
+    for (int r = r0; r < r0 + n; ++r) sc[B_][m][r] = fmaf(sc[B_][m][r], sl2, mneg[m & 1]);
   };
   // Mask of key block j in sc[B_], tile m: key kv0 + k is dropped for query q
   // when k > lim (causal: past q, or for the off-by-one mutant at q; past the
@@ -349,6 +355,8 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
       const float m = swap_max(mx) * sl2;
       mneg[qt] = m == -INFINITY ? 0.f : -m;
     }
+#pragma unroll
+    for (int m = 0; m < 4; ++m) to_log2(0, m, 0, 16);
   }
 
   // Iteration j (C = j % 2): S(j) in sc[C], K(j+1) in K slot 1-C, V(j) in V
@@ -375,10 +383,10 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
         ld_tr_asm<base + 4 * KROW>(vr[ks & 1][3 % NDT][1], vaddr[3 % NDT]);
       }
     };
-    // Region 1: K fragments three k steps ahead; the exponentials run as a
-    // three-stage chain over the slots (FMA of pair e+1, exp of pair e, pack
-    // of pair e-1 after the MFMA of slot e) so no VALU op waits on the one
-    // before it.
+    float ls[2][2] = {{0.f, 0.f}, {0.f, 0.f}};   // row sums of P(j): [qt][parity]
+    // Region 1: K fragments three k steps ahead; after the MFMA of slot e,
+    // the exponentials of pair e and the pack and row sum of pair e-1 (so no
+    // VALU op waits on the one before it).
     {
       bf16x8 kf[4][2];
 #pragma unroll
@@ -386,8 +394,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
         kf[ks][0] = kfrag(N, ks, 0);
         kf[ks][1] = kfrag(N, ks, 1);
       }
-      float pv[3][2];
-      fma_pair(C, 0, pv[0]);
+      float pv[2][2];
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
         if (ks + 3 < NKS) {
@@ -404,12 +411,12 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
           // otherwise also wait for these reads.
           if (ks * 4 + m == R1 - 2) vreads(std::integral_constant<int, 0>{});
           {
+            const int slot = ks * 4 + m;
             // Next blocks' loads, one every R1 / (2 LD) slots: K(j+2) into K
             // slot C (K(j) was read in the previous iteration), V(j+1) into V
             // slot N (V(j-1) likewise); the barrier at the top of this
             // iteration ordered those reads before these writes.
             constexpr int every = R1 / (2 * LD);
-            const int slot = ks * 4 + m;
             if (slot % every == 0) {
               const int q = slot / every;
               if (q < LD) issue1(ksrc, koff, j + 2, smem + C * KB, q);
@@ -419,19 +426,22 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
 #pragma unroll
           for (int i = 0; i < EPS; ++i) {
             const int e = (ks * 4 + m) * EPS + i;          // pair 0..31
-            if (e >= 1) pack_pair(e - 1, pv[(e - 1) % 3]);
-            pv[e % 3][0] = __builtin_amdgcn_exp2f(pv[e % 3][0]);
-            pv[e % 3][1] = __builtin_amdgcn_exp2f(pv[e % 3][1]);
-            if (e + 1 < 32) fma_pair(C, e + 1, pv[(e + 1) % 3]);
+            exp_pair(C, e, pv[e & 1]);
+            if (e >= 1) {
+              pack_pair(e - 1, pv[(e - 1) & 1]);
+              float& l = ls[(e - 1) >> 4][(e - 1) & 1];
+              l += pv[(e - 1) & 1][0] + pv[(e - 1) & 1][1];
+              asm volatile("" : "+v"(l));   // keep the add in this slot
+            }
           }
           fence();
         }
       }
-      pack_pair(31, pv[31 % 3]);
+      pack_pair(31, pv[1]);
+      ls[1][1] += pv[1][0] + pv[1][1];
     }
     // Region 2.
     {
-      float ls[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
       auto kstep = [&](auto KS) {
         constexpr int ks = decltype(KS)::value;
         if constexpr (ks + 1 < 4) {
@@ -452,18 +462,15 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
           const bf16x8 vf = __builtin_bit_cast(
               bf16x8, __builtin_shufflevector(vr[ks & 1][t][0], vr[ks & 1][t][1], 0, 1, 2, 3));
           mma_o(o[t][qt], vf, __builtin_bit_cast(bf16x8, pk[qt][ks]));
-          // Row sums of P(j) in fp32 (the bf16 pairs unpacked by shift and
-          // mask; a dot-product instruction here would stall the MFMAs).
-#pragma unroll
-          for (int i = 0; i < 32 / R2; ++i) {
-            const int d = slot * (32 / R2) + i;                // 0..31
-            const int dq = d >> 4;
-            const uint32_t u = pk[dq][(d >> 2) & 3][d & 3];
-            ls[dq][0] += __uint_as_float(u << 16);
-            ls[dq][1] += __uint_as_float(u & 0xffff0000u);
-            // Keep the adds in this slot (the compiler would otherwise sink
-            // them into one serial chain after the last MFMA).
-            asm volatile("" : "+v"(ls[dq][0]), "+v"(ls[dq][1]));
+          // S(j+1) to log2 units, 64 / R2 registers per slot, tile by tile in
+          // the order its MFMA chains finished (tile 0 three MFMAs before the
+          // end of region 1); pinned here (the compiler would otherwise sink
+          // them to their use in the next iteration).
+          {
+            constexpr int per = 64 / R2;
+            const int t0 = (slot * per) >> 4, r0 = (slot * per) & 15;
+            to_log2(N, t0, r0, per);
+            if (r0 + per == 16) asm volatile("" : "+v"(sc[N][t0]));
           }
           fence();
         }
