@@ -28,6 +28,7 @@ namespace mk {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) char lds_char;
 
 namespace {
 
@@ -248,8 +249,13 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
   auto issue1 = [&](__amdgpu_buffer_rsrc_t src, const uint32_t (&off0)[LD], int j, char* dst,
                     int q) {
     const uint32_t soff = (uint32_t)min(j, n_kv - 1) * BKV * rowb;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * NW + wu) * 1024), 16,
-                                             (int)off0[q], (int)soff, 0, 0);
+    // The wave's 1 KB offset, re-derived at every load so the destination is
+    // one scalar add from it (a table of every destination, hoisted out of
+    // the loop, spills the scalar registers into vector lanes).
+    uint32_t wo = (uint32_t)wu * 1024u;
+    asm volatile("" : "+s"(wo));
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        src, (lds_void*)((lds_char*)dst + wo + q * NW * 1024), 16, (int)off0[q], (int)soff, 0, 0);
   };
   auto issue = [&](__amdgpu_buffer_rsrc_t src, const uint32_t (&off0)[LD], int j, char* dst) {
 #pragma unroll
@@ -318,10 +324,16 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
     const int kmax = min(BKV, Si - kv0);
     const int qrel = qf + qt * 32 + lr - kv0;
     const int lim = CAUSAL ? min(a.causal == 2 ? qrel - 1 : qrel, kmax - 1) : kmax - 1;
+    // All-ones when k > lim, from the sign of lim - k, kept in a vector
+    // register (a compare per register would hold 64 lane masks in scalar
+    // register pairs and spill the loop's scalars).
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int k = kt * 32 + (r >> 3) * 16 + lh * 8 + (r & 7);
-      if (k > lim) sc[B_][m][r] = -INFINITY;
+      uint32_t drop = (uint32_t)((lim - k) >> 31);
+      asm volatile("" : "+v"(drop));
+      const uint32_t v = __float_as_uint(sc[B_][m][r]);
+      sc[B_][m][r] = __uint_as_float((v & ~drop) | (0xff800000u & drop));
     }
   };
 
