@@ -16,6 +16,13 @@
 //    v_mfma_f32_32x32x16_bf16 (fp32: v_mfma_f32_32x32x2_f32), 128 fp32
 //    accumulators per lane.  Conv GEMMs: 256 x 128 tiles, four waves, two
 //    workgroups per CU.
+//  * The four-wave form (bf16 chains without a terminal, K a multiple of 64)
+//    gives each wave a 128 x 128 quarter as 8 x 8 tiles of
+//    v_mfma_f32_16x16x32_bf16.  Same flops per cycle as the 32 x 32 x 16
+//    instruction, but it moves a quarter of the accumulator bytes per
+//    multiply-add (4 registers per 16 x 16 x 32 against 16 per 32 x 32 x 16):
+//    on random operands, with every CU busy, a stream of them holds a clock
+//    about 12% higher under the power limit (2.15 against 1.91 GHz).
 //  * Operands move HBM -> LDS with buffer_load ... lds (no register staging).
 //    An LDS row holds one K stage of one operand row: 128 bytes for plain
 //    GEMMs (64 bf16 / 32 fp32; eight 16-byte chunks), so every 8 lanes of a
@@ -221,6 +228,12 @@ struct SliceLoader {
                                                16, (int)voff[q], (int)soff, 0, 0);
   }
 
+  // Load q of a whole stage (as issue_full).
+  __device__ __forceinline__ void issue_q(char* dst, uint32_t soff, int q) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * WAVES + wid) * 1024), 16,
+                                             (int)voff[q], (int)soff, 0, 0);
+  }
+
   // Rows gathered from arbitrary byte offsets (implicit-GEMM conv: output
   // position m -> its window origin in the padded NHWC input).
   template <typename RowOff>
@@ -326,6 +339,14 @@ __device__ __forceinline__ f32x16 mfma1(const typename MfmaType<T>::frag& x,
   }
 }
 
+// 16 x 16 x 32 MFMA with the accumulator tied to the result in AGPRs (the
+// builtin leaves the compiler free to put them apart, and it then copies
+// accumulators between every use).  The compiler does not see it as an MFMA:
+// the code keeps the distances to readers of the result itself.
+__device__ __forceinline__ void mfma16(f32x4& c, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+
 // vmcnt(n) with the other counters left alone (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vm() {
@@ -356,6 +377,19 @@ __device__ __forceinline__ void stage_slab(const f32x16 (&acc)[4][NJ], float* sl
           f32x4{acc[I][J0 + j][4 * r4], acc[I][J0 + j][4 * r4 + 1], acc[I][J0 + j][4 * r4 + 2],
                 acc[I][J0 + j][4 * r4 + 3]};
     }
+}
+
+// The same slab from the four-wave form's 16 x 16 tiles: acc16[i][j] holds,
+// for column j*16 + l16, the rows i*16 + lq*4 + 0..3 (l16 = lane % 16,
+// lq = lane / 16), which is one 16-byte quad of the slab.
+template <int I, int J0>
+__device__ __forceinline__ void stage_slab16(const f32x4 (&acc16)[8][8], float* slab, int lq,
+                                             int l16) {
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj)
+      *(f32x4*)(slab + ((4 * h + lq) * kSlabU + jj * 16 + l16) * 4) = acc16[2 * I + h][2 * J0 + jj];
 }
 
 // Channel-bias values of one row tile for this lane: rows rb + (r/4)*8 +
@@ -818,20 +852,22 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   bool staged0 = false;   // this tile's stage 0 was issued during the last epilogue
   constexpr int kEpiVmem = sig_plain(SIG) ? 16 * (NJ / 2) : 0;
   // Four-wave form: LDS byte offsets of the A slots (stage ks in ks % 3) and
-  // B slots (ks % 2), and this lane's fragment address bases.  In a wave's
-  // 128 x 128 tile, fragment (i, kk) of A reads row rowbase + i*32 + lr,
-  // logical chunk 2kk + lh, whose physical chunk is (2kk ^ 4(i&1)) ^ X with
-  // X = lh ^ swz(lr) (rowbase and i*32 move the swizzle by 4(i&1) only):
-  // va[kk ^ 2(i&1)] + i*4096 within the slot (likewise B with j).
+  // B slots (ks % 2).
   constexpr int kSlotA3[3] = {0, 65536, 98304};
   constexpr int kSlotB3[2] = {32768, 131072};
-  uint32_t va3[4], vb3[4];
+  // 16 x 16 x 32 fragments: lane (l16, lq) = (lane % 16, lane / 16) of
+  // fragment (t, i) reads row rowbase + i*16 + l16, logical chunk 4t + lq.
+  // With X0 = swz(l16) (i*16 and rowbase move the swizzle by 2(i&3) only) its
+  // physical chunk is lq ^ X0 ^ 2(2t ^ (i&3)): offset va16[2t ^ (i&3)] +
+  // i*2048 within the slot (likewise B with j).
+  uint32_t va16[4], vb16[4];
+  const int l16 = lane & 15, lq = lane >> 4;
   if constexpr (PIPE == 3) {
-    const int X = lh ^ swz<RB>(lr);
+    const int X0 = swz<RB>(l16);
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      va3[c] = (uint32_t)(rowbase * RB + lr * RB + (((2 * c) ^ X) << 4));
-      vb3[c] = (uint32_t)(colbase * RB + lr * RB + (((2 * c) ^ X) << 4));
+    for (int d = 0; d < 4; ++d) {
+      va16[d] = (uint32_t)(rowbase * RB + l16 * RB + ((lq ^ X0 ^ (2 * d)) << 4));
+      vb16[d] = (uint32_t)(colbase * RB + l16 * RB + ((lq ^ X0 ^ (2 * d)) << 4));
     }
   }
   for (;;) {
@@ -839,85 +875,102 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     const bool subt = CONV && PIPE && it.sub >= 0;
     const int rows_it = subt ? SR : BM;
     f32x16 acc[4][NJ];
+    f32x4 acc16[8][8];   // the four-wave form's 16 x 16 tiles
+    if constexpr (PIPE == 3) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
+        for (int j = 0; j < 8; ++j) acc16[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    } else {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    }
 
     if constexpr (PIPE == 3) {
-      // Four waves, one per SIMD, each a 128 x 128 quarter of the tile (4 x 4
-      // MFMA tiles); K a multiple of the 64-deep stage.  Same slot scheme as
-      // the eight-wave form (A of stage ks in slot ks % 3, B in ks % 2; A(ks+2)
-      // issued over sub-steps 0 and 1, B(ks+2) after the stage barrier, which
-      // sits before the last sub-step), with the stage loop unrolled by 6 so
-      // every slot offset is a constant: no address arithmetic per fragment
-      // read, no K-bound select per load (stages past the last read zeros via
-      // the stage offset).
+      // Four waves, one per SIMD, each a 128 x 128 quarter of the tile (8 x 8
+      // tiles of 16 x 16); K a multiple of the 64-deep stage, taken as two
+      // 32-deep steps of 64 MFMAs.  A of stage ks sits in slot ks % 3, B in
+      // ks % 2.  Step 0 runs on fragments read during the previous step and
+      // reads step 1's while A(ks+2) is issued into the slot stage ks-1 held;
+      // then the stage barrier (stage ks+1 landed, this stage's reads done),
+      // and step 1 reads stage ks+1's first fragments while B(ks+2) refills
+      // B slot ks % 2.  The stage loop is unrolled by 6 so every slot offset
+      // is a constant: no address arithmetic per fragment read, no K-bound
+      // select per load (stages past the last read zeros via the stage
+      // offset).
       auto soff3 = [&](int ks, uint32_t range) __attribute__((always_inline)) -> uint32_t {
         return ks < nk ? (uint32_t)ks * RB : range;
       };
-      auto read3 = [&](auto SA_, auto SB_, auto KK_, Frags<NJ, T>& f) __attribute__((always_inline)) {
-        constexpr int SA = decltype(SA_)::value, SB = decltype(SB_)::value;
-        constexpr int KK = decltype(KK_)::value;
-        typedef typename MfmaType<T>::frag F;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          f.a[i] = *(const F*)(smem + kSlotA3[SA] + i * 4096 + va3[KK ^ (2 * (i & 1))]);
-#pragma unroll
-        for (int j = 0; j < NJ; ++j)
-          f.b[j] = *(const F*)(smem + kSlotB3[SB] + j * 4096 + vb3[KK ^ (2 * (j & 1))]);
+      struct F16 {
+        bf16x8 a[8], b[8];
       };
-      // per sub-step: kMfmaSub MFMAs, kReadPairs pairs of fragment reads
-      auto interleave3 = [&](auto NV_) __attribute__((always_inline)) {
-        constexpr int nv = decltype(NV_)::value;
+      auto rd_a = [&](auto SA_, auto T_, int i, bf16x8& d) __attribute__((always_inline)) {
+        constexpr int SA = decltype(SA_)::value, TT = decltype(T_)::value;
+        d = *(const bf16x8*)(smem + kSlotA3[SA] + i * 2048 + va16[(2 * TT) ^ (i & 3)]);
+      };
+      auto rd_b = [&](auto SB_, auto T_, int j, bf16x8& d) __attribute__((always_inline)) {
+        constexpr int SB = decltype(SB_)::value, TT = decltype(T_)::value;
+        d = *(const bf16x8*)(smem + kSlotB3[SB] + j * 2048 + vb16[(2 * TT) ^ (j & 3)]);
+      };
+      // One 32-deep step: 64 MFMAs on `cur`, row by row (A fragment i with
+      // the 8 B fragments), in program order with the reads of the next
+      // step's fragments into `nxt` (step TN of the stage in slots SA / SB):
+      // its 8 B fragments among row 0's MFMAs, its A fragment i after row
+      // i+1's first MFMA (cur.a[i] is dead by then, so the two can share a
+      // register), and the 8 operand loads `ld(q)` in the middle of rows
+      // 1 .. 7 (two in row 7).
+      auto step16 = [&](const F16& cur, F16& nxt, auto SA_, auto SB_, auto TN_, auto ld)
+          __attribute__((always_inline)) {
 #pragma unroll
-        for (int g = 0; g < kReadPairs; ++g) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
+        for (int j = 0; j < 8; ++j) {
+          mfma16(acc16[0][j], cur.a[0], cur.b[j]);
+          rd_b(SB_, TN_, j, nxt.b[j]);
+          __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
-        for (int g = 0; g < nv; ++g) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+        for (int i = 1; i < 8; ++i) {
+          mfma16(acc16[i][0], cur.a[i], cur.b[0]);
+          rd_a(SA_, TN_, i - 1, nxt.a[i - 1]);
+#pragma unroll
+          for (int j = 1; j < 4; ++j) mfma16(acc16[i][j], cur.a[i], cur.b[j]);
+          ld(i - 1);
+          if (i == 7) ld(7);
+#pragma unroll
+          for (int j = 4; j < 8; ++j) mfma16(acc16[i][j], cur.a[i], cur.b[j]);
+          __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, kMfmaSub - kReadPairs - nv, 0);
+        rd_a(SA_, TN_, 7, nxt.a[7]);
         __builtin_amdgcn_sched_barrier(0);
       };
-      Frags<NJ, T> f0, f1;
+      static_assert(LA == 8 && LB == 8, "eight operand loads per wave and step");
+      F16 f0, f1;
       auto stage3 = [&](auto S6_, int ks) __attribute__((always_inline)) {
         constexpr int S6 = decltype(S6_)::value;
         constexpr int SA = S6 % 3, SB = S6 % 2, SA1 = (S6 + 1) % 3, SB1 = (S6 + 1) % 2,
                       SA2 = (S6 + 2) % 3;
         using I0 = std::integral_constant<int, 0>;
         using I1 = std::integral_constant<int, 1>;
-        using I2 = std::integral_constant<int, 2>;
-        using I3 = std::integral_constant<int, 3>;
-        using CA = std::integral_constant<int, SA>;
-        using CB = std::integral_constant<int, SB>;
         const uint32_t sa2 = soff3(ks + 2, la.range), sb2 = soff3(ks + 2, lb.range);
-        read3(CA{}, CB{}, I1{}, f1);
-        la.template issue_full<0, kA0>(smem + kSlotA3[SA2], sa2);
-        mfma_step<NJ, T, false>(f0, acc);
-        interleave3(std::integral_constant<int, kA0>{});
-        read3(CA{}, CB{}, I2{}, f0);
-        la.template issue_full<kA0, LA>(smem + kSlotA3[SA2], sa2);
-        mfma_step<NJ, T, false>(f1, acc);
-        interleave3(std::integral_constant<int, kA1>{});
-        read3(CA{}, CB{}, I3{}, f1);
-        mfma_step<NJ, T, false>(f0, acc);
-        interleave3(std::integral_constant<int, 0>{});
+        // step 0: reads of step 1, A(ks+2) into the slot stage ks-1 held
+        step16(f0, f1, std::integral_constant<int, SA>{}, std::integral_constant<int, SB>{}, I1{},
+               [&](int q) __attribute__((always_inline)) {
+                 la.issue_q(smem + kSlotA3[SA2], sa2, q);
+               });
         // stage ks+1 landed (only A(ks+2) may remain) and this wave's reads
         // of stage ks are done; the barrier makes both hold for every wave
         wait_vm<LA>();
         __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
-        read3(std::integral_constant<int, SA1>{}, std::integral_constant<int, SB1>{}, I0{}, f0);
-        lb.template issue_full<0, LB>(smem + kSlotB3[SB], sb2);
-        mfma_step<NJ, T, false>(f1, acc);
-        interleave3(std::integral_constant<int, LB>{});
+        // step 1: reads of stage ks+1's step 0, B(ks+2) into B slot ks % 2
+        step16(f1, f0, std::integral_constant<int, SA1>{}, std::integral_constant<int, SB1>{},
+               I0{}, [&](int q) __attribute__((always_inline)) {
+                 lb.issue_q(smem + kSlotB3[SB], sb2, q);
+               });
       };
       if (!staged0) {
         la.template issue_full<0, LA>(smem + kSlotA3[0], 0u);
@@ -930,8 +983,12 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       else
         wait_vm<LA + LB>();
       __builtin_amdgcn_s_barrier();
-      read3(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{},
-            std::integral_constant<int, 0>{}, f0);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        rd_b(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{}, j, f0.b[j]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        rd_a(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{}, i, f0.a[i]);
       int ks = 0;
       for (; ks + 6 <= nk; ks += 6) {
         stage3(std::integral_constant<int, 0>{}, ks);
@@ -946,6 +1003,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       if (ks + 2 < nk) stage3(std::integral_constant<int, 2>{}, ks + 2);
       if (ks + 3 < nk) stage3(std::integral_constant<int, 3>{}, ks + 3);
       if (ks + 4 < nk) stage3(std::integral_constant<int, 4>{}, ks + 4);
+      // the last MFMAs finish before the epilogue reads their results
+      asm volatile("s_nop 15\n\ts_nop 15" ::: "memory");
     } else if (PIPE && subt) {
       // Row sub-tile: waves wm with wm*32 < SR compute rows wm*32 .. +31 of
       // it into acc[0]; every wave loads.  Three stages in flight; one
@@ -1126,7 +1185,17 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     const int lane_e = tid_e & 63, w_e = tid_e >> 6;
     const int wn_e = w_e % WN;
     const int lr = lane_e & 31, lh = lane_e >> 5;
+    const int l16e = lane_e & 15, lqe = lane_e >> 4;
     const int rowbase = (w_e / WN) * (subt ? 32 : 128), colbase = wn_e * WTN;
+    // 32-row slab I of 64 columns J0*32 .. J0*32+63 of this wave's tile from
+    // the accumulators, in either MFMA layout.
+    auto stage_any = [&](auto I_, auto J0_, float* sl) __attribute__((always_inline)) {
+      constexpr int I = decltype(I_)::value, J0 = decltype(J0_)::value;
+      if constexpr (PIPE == 3)
+        stage_slab16<I, J0>(acc16, sl, lqe, l16e);
+      else
+        stage_slab<I, NJ, J0>(acc, sl, lh, lr);
+    };
     // Epilogue lane roles: 8-column group q and row group rg of the slab;
     // the 8 lanes of a row (same rg) are lanes rg, rg+8, ..., rg+56.
     const int q = lane_e >> 3, rg = lane_e & 7;
@@ -1135,7 +1204,9 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
 
     // ---------------------------------------------------------------- epilogue
     // acc[i][j][r] is C[row, col] with
-    //   row = m0 + rowbase + i*32 + (r/4)*8 + lh*4 + r%4,  col = n0 + colbase + j*32 + lr.
+    //   row = m0 + rowbase + i*32 + (r/4)*8 + lh*4 + r%4,  col = n0 + colbase + j*32 + lr
+    // (four-wave form: acc16[i][j][r] with row = m0 + rowbase + i*16 + lq*4 + r,
+    // col = n0 + colbase + j*16 + l16).
     // Each wave stages one 32-row slab at a time in its own LDS region; lane
     // (q, rg) then reads rows 4rg .. 4rg+3 of columns 8q .. 8q+7, applies the
     // chain to each row's 8 values and writes them with one 16-byte store.
@@ -1404,10 +1475,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
           constexpr int P = decltype(P_)::value;
           if constexpr (P < 8) {
             float* sl = (P & 1) ? slab1 : slab;
-            if constexpr ((P & 1) == 0)
-              stage_slab<P / 2, NJ, 0>(acc, sl, lh, lr);
-            else
-              stage_slab<P / 2, NJ, 2>(acc, sl, lh, lr);
+            stage_any(std::integral_constant<int, P / 2>{},
+                      std::integral_constant<int, (P & 1) ? 2 : 0>{}, sl);
           }
           __builtin_amdgcn_wave_barrier();
         };
@@ -1474,13 +1543,14 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         }
         u32x4 ra[4], rb[4];
         if constexpr (SIG == kSigAdd) load_res(0, ra);
-        stage_slab<0, NJ, 2 * H>(acc, slab, lh, lr);
+        using J = std::integral_constant<int, 2 * H>;
+        stage_any(std::integral_constant<int, 0>{}, J{}, slab);
         finish_slab_sig(std::integral_constant<int, 0>{}, ra, rb);
-        stage_slab<1, NJ, 2 * H>(acc, slab, lh, lr);
+        stage_any(std::integral_constant<int, 1>{}, J{}, slab);
         finish_slab_sig(std::integral_constant<int, 1>{}, rb, ra);
-        stage_slab<2, NJ, 2 * H>(acc, slab, lh, lr);
+        stage_any(std::integral_constant<int, 2>{}, J{}, slab);
         finish_slab_sig(std::integral_constant<int, 2>{}, ra, rb);
-        stage_slab<3, NJ, 2 * H>(acc, slab, lh, lr);
+        stage_any(std::integral_constant<int, 3>{}, J{}, slab);
         finish_slab_sig(std::integral_constant<int, 3>{}, rb, ra);
       };
       half(std::integral_constant<int, 0>{});
