@@ -918,33 +918,34 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       };
       // One 32-deep step: 64 MFMAs on `cur`, row by row (A fragment i with
       // the 8 B fragments), in program order with the reads of the next
-      // step's fragments into `nxt` (step TN of the stage in slots SA / SB):
-      // its 8 B fragments among row 0's MFMAs, its A fragment i after row
-      // i+1's first MFMA (cur.a[i] is dead by then, so the two can share a
-      // register), and the 8 operand loads `ld(q)` in the middle of rows
-      // 1 .. 7 (two in row 7).
+      // step's 16 fragments into `nxt` (step TN of the stage in slots SA /
+      // SB) and the 8 operand loads `ld(q)` in rows 0 .. 3 (per row four
+      // reads and two loads): the reads have returned long before the end of
+      // the step, where the stage barrier waits for them.
       auto step16 = [&](const F16& cur, F16& nxt, auto SA_, auto SB_, auto TN_, auto ld)
           __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          mfma16(acc16[0][j], cur.a[0], cur.b[j]);
-          rd_b(SB_, TN_, j, nxt.b[j]);
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            mfma16(acc16[i][j], cur.a[i], cur.b[j]);
+            if (j & 1) {
+              const int r = i * 4 + (j >> 1);   // read 0..15: B 0..7, then A 0..7
+              if (r < 8)
+                rd_b(SB_, TN_, r, nxt.b[r]);
+              else
+                rd_a(SA_, TN_, r - 8, nxt.a[r - 8]);
+            }
+            if (j == 2 || j == 6) ld(2 * i + (j >> 2));
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
-        for (int i = 1; i < 8; ++i) {
-          mfma16(acc16[i][0], cur.a[i], cur.b[0]);
-          rd_a(SA_, TN_, i - 1, nxt.a[i - 1]);
+        for (int i = 4; i < 8; ++i) {
 #pragma unroll
-          for (int j = 1; j < 4; ++j) mfma16(acc16[i][j], cur.a[i], cur.b[j]);
-          ld(i - 1);
-          if (i == 7) ld(7);
-#pragma unroll
-          for (int j = 4; j < 8; ++j) mfma16(acc16[i][j], cur.a[i], cur.b[j]);
+          for (int j = 0; j < 8; ++j) mfma16(acc16[i][j], cur.a[i], cur.b[j]);
           __builtin_amdgcn_sched_barrier(0);
         }
-        rd_a(SA_, TN_, 7, nxt.a[7]);
-        __builtin_amdgcn_sched_barrier(0);
       };
       static_assert(LA == 8 && LB == 8, "eight operand loads per wave and step");
       F16 f0, f1;
