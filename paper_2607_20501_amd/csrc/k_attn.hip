@@ -372,10 +372,16 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
   }
 
   // Iteration j (C = j % 2): S(j) in sc[C], K(j+1) in K slot 1-C, V(j) in V
-  // slot C.  On a wave's last block the S(j+1) products run on whatever the
-  // slot holds and are never read.
-  auto iter = [&](int j, auto PAR) {
+  // slot C.  On a wave's last block (LAST) there is no S(j+1): region 1 is
+  // the exponentials alone, region 2 the PV products alone, and the wave's
+  // share of the workgroup's next loads goes out at the top.
+  auto iter = [&](int j, auto PAR, auto LAST_) {
     constexpr int C = decltype(PAR)::value, N = 1 - C;
+    constexpr bool LAST = decltype(LAST_)::value;
+    if constexpr (LAST) {
+      issue(ksrc, koff, j + 2, smem + C * KB);
+      issue(vsrc, voff, j + 1, smem + (2 + N) * KB);
+    }
     fence();
     // V^T fragments of one k step of region 2: 2 transposing reads per dh
     // tile, issued one k step ahead; lds_wait<2*NDT> before a step's MFMAs
@@ -401,22 +407,26 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
     // VALU op waits on the one before it).
     {
       bf16x8 kf[4][2];
+      if constexpr (!LAST) {
 #pragma unroll
-      for (int ks = 0; ks < 3; ++ks) {
-        kf[ks][0] = kfrag(N, ks, 0);
-        kf[ks][1] = kfrag(N, ks, 1);
+        for (int ks = 0; ks < 3; ++ks) {
+          kf[ks][0] = kfrag(N, ks, 0);
+          kf[ks][1] = kfrag(N, ks, 1);
+        }
       }
       float pv[2][2];
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
-        if (ks + 3 < NKS) {
+        if (!LAST && ks + 3 < NKS) {
           kf[(ks + 3) & 3][0] = kfrag(N, ks + 3, 0);
           kf[(ks + 3) & 3][1] = kfrag(N, ks + 3, 1);
         }
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
-          if (ks == 0) mma_s0(sc[N][m], kf[ks & 3][m >> 1], qfr[m & 1][ks]);
-          else mma_s(sc[N][m], kf[ks & 3][m >> 1], qfr[m & 1][ks]);
+          if constexpr (!LAST) {
+            if (ks == 0) mma_s0(sc[N][m], kf[ks & 3][m >> 1], qfr[m & 1][ks]);
+            else mma_s(sc[N][m], kf[ks & 3][m >> 1], qfr[m & 1][ks]);
+          }
           // The first V^T reads of region 2 (V(j) has been in LDS since the
           // top of this iteration), two slots before the region ends: after
           // the compiler's wait for the last K fragment, which would
@@ -429,7 +439,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
             // slot N (V(j-1) likewise); the barrier at the top of this
             // iteration ordered those reads before these writes.
             constexpr int every = R1 / (2 * LD);
-            if (slot % every == 0) {
+            if (!LAST && slot % every == 0) {
               const int q = slot / every;
               if (q < LD) issue1(ksrc, koff, j + 2, smem + C * KB, q);
               else issue1(vsrc, voff, j + 1, smem + (2 + N) * KB, q - LD);
@@ -478,7 +488,7 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
           // the order its MFMA chains finished (tile 0 three MFMAs before the
           // end of region 1); pinned here (the compiler would otherwise sink
           // them to their use in the next iteration).
-          {
+          if constexpr (!LAST) {
             constexpr int per = 64 / R2;
             const int t0 = (slot * per) >> 4, r0 = (slot * per) & 15;
             to_log2(N, t0, r0, per);
@@ -493,9 +503,19 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
       kstep(std::integral_constant<int, 3>{});
       // Mask of S(j+1) when block j+1 is the wave's last (causal diagonal /
       // sequence end); 32 MFMAs after its last product.
-      if (j + 2 >= nb_w) {
+      if (!LAST && j + 2 >= nb_w) {
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) mask_tile(N, j + 1, mt);
+      }
+      if constexpr (LAST) {
+        // O's last products: the compiler does not see these MFMAs and
+        // would copy O out of the AGPRs right behind them; drain first, then
+        // redefine O so that every copy comes after the drain.
+        mfma_drain();
+#pragma unroll
+        for (int t = 0; t < NDT; ++t)
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) asm volatile("" : "+a"(o[t][qt]));
       }
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
@@ -518,16 +538,26 @@ __global__ __launch_bounds__(64 * NW, 1) void attn_fwd_pipe_kernel(AttnArgs a) {
     issue(ksrc, koff, j + 2, smem + par * KB);
     issue(vsrc, voff, j + 1, smem + (3 - par) * KB);
   };
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  using Full = std::integral_constant<bool, false>;
+  using Last = std::integral_constant<bool, true>;
   int j = 0;
-  for (; j + 1 < nb_w; j += 2) {
+  for (; j + 2 < nb_w; j += 2) {
     top(j);
-    iter(j, std::integral_constant<int, 0>{});
+    iter(j, P0{}, Full{});
     top(j + 1);
-    iter(j + 1, std::integral_constant<int, 1>{});
+    iter(j + 1, P1{}, Full{});
   }
-  if (j < nb_w) {
+  if (nb_w - j == 2) {
     top(j);
-    iter(j, std::integral_constant<int, 0>{});
+    iter(j, P0{}, Full{});
+    top(j + 1);
+    iter(j + 1, P1{}, Last{});
+    j += 2;
+  } else if (nb_w - j == 1) {
+    top(j);
+    iter(j, P0{}, Last{});
     ++j;
   }
   for (; j < n_kv; ++j) top_idle(j, j & 1);
