@@ -104,17 +104,36 @@ def measured_traffic(workload, kernel):
     return rec["hbm_bytes_per_launch"]
 
 
-def time_module(mod, ins, out, ws, steps, warmup):
-    """ms per step over `steps` back-to-back runs (after `warmup` untimed
-    ones), bracketed by device synchronisation; then, for each launch k of a
-    run, `steps` more runs with a HIP event pair around launch k alone (the
-    other launches run back to back, as in the timed steps) for per-launch
-    durations.  An event pair adds the launch's dispatch time (a few
-    microseconds) to its figure, so the pairs stay out of the timed region."""
+def warmup_steps(mod, ins, out, ws, warmup):
+    """Run the untimed warm-up: exactly `warmup` steps when given, otherwise
+    at least 10 steps and at least 100 ms of them (after an idle period the
+    chip needs tens of milliseconds under load to reach its steady clock;
+    10 steps of a 250-us module are 2.5 ms).  Returns the count run."""
     import torch
-    for _ in range(warmup):
-        mod.run(ins, out, ws)
-    torch.cuda.synchronize()
+    if warmup is not None:
+        for _ in range(warmup):
+            mod.run(ins, out, ws)
+        torch.cuda.synchronize()
+        return warmup
+    n, t0 = 0, time.perf_counter()
+    while n < 10 or time.perf_counter() - t0 < 0.1:
+        for _ in range(10):
+            mod.run(ins, out, ws)
+        n += 10
+        torch.cuda.synchronize()
+    return n
+
+
+def time_module(mod, ins, out, ws, steps, warmup):
+    """ms per step over `steps` back-to-back runs (after the untimed warm-up,
+    see warmup_steps), bracketed by device synchronisation; then, for each
+    launch k of a run, `steps` more runs with a HIP event pair around launch k
+    alone (the other launches run back to back, as in the timed steps) for
+    per-launch durations.  An event pair adds the launch's dispatch time (a
+    few microseconds) to its figure, so the pairs stay out of the timed
+    region.  Returns (ms, per-launch ms, warm-up steps run)."""
+    import torch
+    warmed = warmup_steps(mod, ins, out, ws, warmup)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
     for _ in range(steps):
@@ -130,7 +149,7 @@ def time_module(mod, ins, out, ws, steps, warmup):
         torch.cuda.synchronize()
         launch_ms = mod.profile_end(steps)
         per_launch.append(sum(launch_ms) / len(launch_ms))
-    return ms, per_launch
+    return ms, per_launch, warmed
 
 
 def median_flushed(mod, ins, out, ws, runs, flush):
@@ -221,7 +240,9 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed warm-up steps (default: at least 10 and at least 100 ms of "
+                         "steps, so that the chip has reached its steady clock)")
     ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--dtype", default=None, choices=[None, "f32", "bf16"])
     ap.add_argument("--decomp", default="fused", choices=["fused", "split"])
@@ -267,13 +288,13 @@ def main():
         log(f"calibration copy: {n} bytes")
         del src, dst
 
-    ms, per_launch = time_module(fused, ins, out, ws, args.steps, args.warmup)
+    ms, per_launch, warmed = time_module(fused, ins, out, ws, args.steps, args.warmup)
     log(f"{args.decomp}: {ms * 1e3:.1f} us/step, launches (us): "
         f"{[round(x * 1e3, 1) for x in per_launch]}")
     result = {}
     if split is not None:
         out_s = mk.out_tensor(module, split.info["out_shape"])
-        ms_s, per_s = time_module(split, ins, out_s, ws, args.steps, args.warmup)
+        ms_s, per_s, _ = time_module(split, ins, out_s, ws, args.steps, args.warmup)
         log(f"split: {ms_s * 1e3:.1f} us/step, launches (us): {[round(x * 1e3, 1) for x in per_s]}")
         result["split"] = {"ms_per_step": ms_s, "value": flops / (ms_s * 1e-3) / 1e12,
                            "launch_us": [round(x * 1e3, 2) for x in per_s]}
@@ -334,7 +355,7 @@ def main():
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": warmed,
         "ms_per_step": ms,
         "higher_is_better": True,
         "scaling": "weak",
