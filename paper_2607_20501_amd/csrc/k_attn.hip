@@ -98,7 +98,11 @@ constexpr float kOverflowSum = 274877906944.0f;   // 2^38
 // Matrix-core products with the register file of every operand fixed.  The
 // compiler does not model these as MFMAs, so the code keeps the required
 // distance between an MFMA and a VALU read of its result itself (other MFMAs
-// in between, or mfma_drain()).
+// in between, or mfma_drain()).  Nor does it keep the two wait states an MFMA
+// needs after a VALU write of one of its sources: where it moves O between
+// accumulator registers (a block whose register assignment differs from the
+// loop's) the move can sit right before the product, so the O product starts
+// with those two wait states itself.
 __device__ __forceinline__ void mma_s0(f32x16& d, const bf16x8& k, const bf16x8& q) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(k), "a"(q));
 }
@@ -106,7 +110,7 @@ __device__ __forceinline__ void mma_s(f32x16& d, const bf16x8& k, const bf16x8& 
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(k), "a"(q));
 }
 __device__ __forceinline__ void mma_o(f32x16& o, const bf16x8& v, const bf16x8& p) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(v), "v"(p));
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(v), "v"(p));
 }
 __device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 15\n\ts_nop 15" ::: "memory"); }
 // Transposing LDS read issued as asm: the compiler would otherwise wait for
