@@ -1436,13 +1436,17 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
                                                        subt ? (rowbase < SR ? 1 : 0) : 4);
     } else if (PIPE == 3 && m0 + BM <= a.M && n0 + BN <= a.N && vec_ok) {
       // Four-wave form, whole tile: the 8 passes (32-row slab I, 64-column
-      // half H) alternate between the wave's two slabs, the next pass staged
-      // before the current one is read back (LDS operations of a wave run in
-      // order, so only the compiler's ordering needs a fence); a lane
-      // finishes rows rowbase + I*32 + rg*4 + t of columns colbase + H*64 +
-      // q*8 .. +7.  No row or column bounds, 32-bit offsets stepping by rows,
-      // one 16-byte store per row; residual pieces are requested two passes
-      // ahead.
+      // half H) alternate between the wave's two slabs; a pass reads its
+      // slab back and then stages the next pass into the other one, so the
+      // reads wait for nothing behind them and the staging overlaps this
+      // pass's arithmetic and stores (LDS operations of a wave run in order,
+      // so only the compiler's ordering needs a fence; the next staging into
+      // this slab comes after these reads).  A lane finishes rows rowbase +
+      // I*32 + rg*4 + t of columns colbase + H*64 + q*8 .. +7.  No row or
+      // column bounds, 32-bit offsets stepping by rows, one 16-byte store per
+      // row; residual pieces are requested two passes ahead.  The passes
+      // exist twice, with and without the alpha multiply (alpha is 1 in most
+      // modules: one VALU operation per value less).
       if constexpr (PIPE == 3) {
         const float alpha = a.alpha;
         const uint32_t ldc2 = (uint32_t)a.ldc * 2u;
@@ -1477,15 +1481,16 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
           }
           __builtin_amdgcn_wave_barrier();
         };
-        auto pass3 = [&](auto P_) __attribute__((always_inline)) {
+        auto pass3 = [&](auto P_, auto UA_) __attribute__((always_inline)) {
           constexpr int P = decltype(P_)::value;
-          stage3(std::integral_constant<int, P + 1>{});
-          load_res3(std::integral_constant<int, P + 2>{});
+          constexpr bool UA = decltype(UA_)::value;   // alpha == 1
           const float* sl = (P & 1) ? slab1 : slab;
           f32x4 u[8];
 #pragma unroll
           for (int k = 0; k < 8; ++k) u[k] = *(const f32x4*)(sl + (rg * kSlabU + q * 8 + k) * 4);
           __builtin_amdgcn_wave_barrier();
+          stage3(std::integral_constant<int, P + 1>{});
+          load_res3(std::integral_constant<int, P + 2>{});
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
             float v[8];
@@ -1493,13 +1498,13 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
             for (int e = 0; e < 8; ++e) {
               const float x = u[e][t];
               if constexpr (SIG == kSigBiasGeluTanhScale)
-                v[e] = gelu_tanh(fmaf(x, alpha, bc[P & 1][e])) * a.epi.s[2];
+                v[e] = gelu_tanh(UA ? x + bc[P & 1][e] : fmaf(x, alpha, bc[P & 1][e])) * a.epi.s[2];
               else if constexpr (SIG == kSigBias)
-                v[e] = fmaf(x, alpha, bc[P & 1][e]);
+                v[e] = UA ? x + bc[P & 1][e] : fmaf(x, alpha, bc[P & 1][e]);
               else if constexpr (SIG == kSigGeluErf)
-                v[e] = gelu_erf_bf16out(x * alpha);
+                v[e] = gelu_erf_bf16out(UA ? x : x * alpha);
               else
-                v[e] = x * alpha;
+                v[e] = UA ? x : x * alpha;
             }
             if constexpr (SIG == kSigAdd) {
               const u32x4 r = res[P % 3][t];
@@ -1518,14 +1523,20 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         stage3(std::integral_constant<int, 0>{});
         load_res3(std::integral_constant<int, 0>{});
         load_res3(std::integral_constant<int, 1>{});
-        pass3(std::integral_constant<int, 0>{});
-        pass3(std::integral_constant<int, 1>{});
-        pass3(std::integral_constant<int, 2>{});
-        pass3(std::integral_constant<int, 3>{});
-        pass3(std::integral_constant<int, 4>{});
-        pass3(std::integral_constant<int, 5>{});
-        pass3(std::integral_constant<int, 6>{});
-        pass3(std::integral_constant<int, 7>{});
+        auto passes = [&](auto UA) __attribute__((always_inline)) {
+          pass3(std::integral_constant<int, 0>{}, UA);
+          pass3(std::integral_constant<int, 1>{}, UA);
+          pass3(std::integral_constant<int, 2>{}, UA);
+          pass3(std::integral_constant<int, 3>{}, UA);
+          pass3(std::integral_constant<int, 4>{}, UA);
+          pass3(std::integral_constant<int, 5>{}, UA);
+          pass3(std::integral_constant<int, 6>{}, UA);
+          pass3(std::integral_constant<int, 7>{}, UA);
+        };
+        if (alpha == 1.f)
+          passes(std::true_type{});
+        else
+          passes(std::false_type{});
       }
     } else if constexpr (sig_plain(SIG)) {
       // (The softmax-partial chain keeps the rolled loop: unrolled, its
