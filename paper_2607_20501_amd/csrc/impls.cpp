@@ -110,6 +110,42 @@ static bool use_mfma(const Plan& p, const Subkernel& sk, int impl) {
   return gemm_mfma_supported(p.dtype, gemm_probe(sk));
 }
 
+static EpiDev resolve(const EpiChain& c, const std::vector<void*>& vals, int impl);
+
+// A softmax terminal over rows one wave holds: the MFMA GEMM writes the
+// chain's values and a one-wave-per-row softmax runs after it in place.
+static bool row_softmax_after(const Plan& p, const GemmSpec& g, bool mfma, const void* out,
+                              RowArgs* rs_out) {
+  if (!(mfma && g.terminal == TERM_SOFTMAX && g.batch * g.heads == 1 && g.ldc == g.N)) return false;
+  RowArgs rs{};
+  char* c0 = (char*)out + g.c_off * elem_size(p.dtype);
+  rs.x = c0;
+  rs.y = c0;
+  rs.rows = g.M;
+  rs.len = g.N;
+  rs.op = MK_OP_SOFTMAX;
+  rs.pre.last = rs.pre.S = rs.pre.C = rs.pre.HW = 1;
+  rs.n2 = 1;
+  if (rs_out) *rs_out = rs;
+  return row_wave_supported(p.dtype, rs);
+}
+
+// A [K, N] weight the MFMA GEMM reads in place (no transpose launch); decided
+// from the spec (the chain's steps, a 16-byte aligned bias assumed: the
+// launch rejects an unaligned one).
+static bool gemm_native_kn(const Plan& p, const Subkernel& sk, int impl) {
+  const GemmSpec& g = sk.gemm;
+  if (!use_mfma(p, sk, impl) || g.layout != 1) return false;
+  GemmArgs a = gemm_probe(sk);
+  int nv = 1;
+  for (int i = 0; i < g.epi.n; ++i) nv = std::max(nv, g.epi.step[i].value + 1);
+  std::vector<void*> dummy((size_t)nv, (void*)256);
+  a.epi = resolve(g.epi, dummy, impl);
+  a.alpha = g.alpha;
+  if (row_softmax_after(p, g, true, nullptr, nullptr)) a.terminal = TERM_NONE;
+  return gemm_mfma_native_kn(p.dtype, a);
+}
+
 static int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
 
 // Scratch layout of a GEMM subkernel: [LayerNorm region][row partials].
@@ -128,7 +164,8 @@ static GemmScratch gemm_scratch(const Plan& p, const Subkernel& sk, int impl) {
   s.tile_n = s.mfma ? gemm_mfma_tile_n(p.dtype, gemm_probe(sk)) : 64;
   s.n_tiles = (g.N + s.tile_n - 1) / s.tile_n;
   if (g.ln) s.ln_bytes = align256(s.mfma ? g.M * g.K * elem_size(p.dtype) : 2 * g.M * 4);
-  if (s.mfma && g.layout == 1) s.bt_bytes = align256(g.batch * g.heads * g.N * g.K * elem_size(p.dtype));
+  if (s.mfma && g.layout == 1 && !gemm_native_kn(p, sk, impl))
+    s.bt_bytes = align256(g.batch * g.heads * g.N * g.K * elem_size(p.dtype));
   if (g.terminal == TERM_ROWSUM) s.partial_bytes = align256(g.M * s.n_tiles * 4);
   if (g.terminal == TERM_SOFTMAX || g.terminal == TERM_LAYERNORM)
     s.partial_bytes = align256(g.M * s.n_tiles * 8);
@@ -191,7 +228,7 @@ int tuned_limit(const Plan& p, const Subkernel& sk) {
 
 int impl_launches(const Plan& p, const Subkernel& sk, int impl) {
   if (sk.family == MK_FAM_GEMM) {
-    const bool transpose = use_mfma(p, sk, impl) && sk.gemm.layout == 1;
+    const bool transpose = use_mfma(p, sk, impl) && sk.gemm.layout == 1 && !gemm_native_kn(p, sk, impl);
     return 1 + (sk.gemm.ln ? 1 : 0) + (transpose ? 1 : 0) +
            (sk.gemm.terminal != TERM_NONE ? 1 : 0);
   }
@@ -341,19 +378,10 @@ mk_status run_subkernel(const Plan& p, const Subkernel& sk, const std::vector<vo
       // the partials' finisher, and no softmax work in the GEMM epilogue).
       // Otherwise the epilogue emits per-tile partials for the finisher.
       RowArgs rs{};
-      bool row_softmax = false;
-      if (gs.mfma && g.terminal == TERM_SOFTMAX && g.batch * g.heads == 1 && g.ldc == g.N) {
-        char* c0 = (char*)out + g.c_off * elem_size(p.dtype);
-        rs.x = c0;
-        rs.y = c0;
-        rs.rows = g.M;
-        rs.len = g.N;
-        rs.op = MK_OP_SOFTMAX;
-        rs.pre.last = rs.pre.S = rs.pre.C = rs.pre.HW = 1;
-        rs.n2 = 1;
-        row_softmax = row_wave_supported(dt, rs);
-      }
+      const bool row_softmax = row_softmax_after(p, g, gs.mfma, out, &rs);
       if (row_softmax) a.terminal = TERM_NONE;
+      if (gs.mfma && a.layout == 1 && !gs.bt_bytes && !gemm_mfma_native_kn(dt, a))
+        return fail(MK_E_INVALID_ARG, "GEMM chain operands must be 16-byte aligned");
       mk_status s = hip_check(timed([&] {
                                 return gs.mfma ? launch_gemm_mfma(dt, a, st)
                                                : launch_gemm_simple(dt, a, st);

@@ -59,6 +59,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 namespace {
 
@@ -279,6 +280,51 @@ struct SliceLoader {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * WAVES + w) * 1024),
                                                16, (int)(in_k ? voff[q] : kOob), (int)soff, 0,
                                                0);
+  }
+};
+
+// Direct HBM -> LDS loads of one stage of a [K, N] bf16 operand for the
+// four-wave form: 64 k-rows of the tile's 256 columns, 512 bytes per row.
+// Row r of the stage sits at r * 512 in the slot with its 16-byte chunks
+// XOR-swizzled by 2 g(r), g(r) = (r & 3) | ((r >> 3) & 1) << 2: the 8 rows
+// that half a wave's transposing fragment reads touch together (rows 0..3
+// and 8..11 of a 16-row group) then lie in 8 distinct 32-byte bank windows.
+// Load q of wave w fills rows 8q + 2w and 8q + 2w + 1 (lanes 0..31, 32..63):
+// lane i writes LDS chunk i % 32 of its row, the row's logical chunk
+// (i % 32) ^ 2 g(row).  Columns past N read zeros (offset out of range); K
+// is a multiple of the stage depth.
+struct KNLoader {
+  __amdgpu_buffer_rsrc_t src;
+  uint32_t voff[8];   // byte offset of load q at k0 = 0 (kOob past N)
+  uint32_t range;     // bytes covered by src
+  uint32_t kstep;     // bytes per stage along K (64 rows)
+  int wid;
+
+  __device__ __forceinline__ void init(const bf16* base, int64_t K, int64_t ld, int64_t n0,
+                                       int64_t N) {
+    range = (uint32_t)(K * ld * 2);
+    kstep = (uint32_t)(64 * ld * 2);
+    src = make_rsrc(base, K * ld * 2);
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    wid = __builtin_amdgcn_readfirstlane(w);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int r = 8 * q + 2 * w + (lane >> 5);
+      const int g = (r & 3) | (((r >> 3) & 1) << 2);
+      const int64_t n = n0 + (int64_t)(((lane & 31) ^ (2 * g)) * 8);
+      voff[q] = n < N ? (uint32_t)(r * ld * 2 + n * 2) : kOob;
+    }
+  }
+  template <int Q0, int Q1>
+  __device__ __forceinline__ void issue_full(char* dst, uint32_t soff) const {
+#pragma unroll
+    for (int q = Q0; q < Q1; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * 4 + wid) * 1024), 16,
+                                               (int)voff[q], (int)soff, 0, 0);
+  }
+  __device__ __forceinline__ void issue_q(char* dst, uint32_t soff, int q) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void*)(dst + (q * 4 + wid) * 1024), 16,
+                                             (int)voff[q], (int)soff, 0, 0);
   }
 };
 
@@ -662,14 +708,14 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   // reuses the top of the LDS (clear of A0 and B0, which take the next tile's
   // stage 0 meanwhile).  Ring form: stage slots back to back, the epilogue
   // from 0.
-  static_assert(WTN == 64 || (PIPE == 3 && WTN == 128),
+  static_assert(WTN == 64 || (PIPE >= 3 && WTN == 128),
                 "the epilogue maps 8 row groups x 8 column groups onto 64 columns of a wave");
-  static_assert(PIPE != 3 || (!CONV && WN == 2 && BN == 256 && RB == 128 && sizeof(T) == 2 &&
+  static_assert(PIPE < 3 || (!CONV && WN == 2 && BN == 256 && RB == 128 && sizeof(T) == 2 &&
                               sig_plain(SIG)),
                 "the four-wave form runs plain bf16 GEMMs with a compiled chain, no terminal");
   constexpr int kRing = PIPE ? 5 * 32768 : kStages * kStageBytes;
   // (the four-wave epilogue alternates between two slabs per wave)
-  constexpr int kSlabs = PIPE == 3 ? 2 : 1;
+  constexpr int kSlabs = PIPE >= 3 ? 2 : 1;
   constexpr int kEpiOff = PIPE ? ((kRing - epi_bytes<WN, BN, kSlabs>()) & ~1023) : 0;
   static_assert(PIPE == 0 || kEpiOff >= 65536, "the epilogue must leave A0 and B0 free");
   constexpr int kEpiEnd = kEpiOff + epi_bytes<WN, BN, kSlabs>();
@@ -717,7 +763,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   const int64_t PQ = a.cv_P * a.cv_Q;
 
   SliceLoader<WAVES, BM, T, RB> la;
-  SliceLoader<WAVES, BN, T, RB> lb;
+  std::conditional_t<PIPE == 4, KNLoader, SliceLoader<WAVES, BN, T, RB>> lb;
   auto init_loaders = [&](const Item& it) {
     const int64_t m0 = row0_of(it), n0 = (int64_t)it.tc.tn * BN;
     la.init(A, it.sub < 0 ? a.M : min<int64_t>(a.M, m0 + SR), a.lda, m0);
@@ -733,6 +779,8 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         const uint32_t p = pq / Qu, q = pq - p * Qu;
         return ((n * Hpu + p * st) * Wpu + q * st) * Cu * (uint32_t)sizeof(T);
       });
+    } else if constexpr (PIPE == 4) {
+      lb.init((const bf16*)B, a.K, a.ldb, n0, a.N);
     } else {
       lb.init(B, a.N, a.ldb, n0);
     }
@@ -753,10 +801,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   // Loads of stage ks (stages past the last read zeros: every lane's K bound
   // fails).
   auto issue_a = [&](int ks) {
-    if constexpr (PIPE != 3) la.issue(a_slot(ks), (int64_t)ks * BK, a.K);
+    if constexpr (PIPE < 3) la.issue(a_slot(ks), (int64_t)ks * BK, a.K);
   };
   auto issue_b = [&](int ks) {
-    if constexpr (PIPE != 3) {
+    if constexpr (PIPE < 3) {
       const int64_t k0 = (int64_t)ks * BK;
       if (CONV)
         lb.issue(b_slot(ks), k0, a.K, conv_koff<T>(a, k0));
@@ -770,7 +818,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   auto a_slot_s = [&](int ks) -> char* { return smem + (ks & 3) * 8192; };
   auto b_slot_s = [&](int ks) -> char* { return smem + 32768 + (ks & 3) * 32768; };
   auto issue_sub = [&](int ks) {
-    if constexpr (PIPE != 3) {
+    if constexpr (PIPE < 3) {
       const int64_t k0 = (int64_t)ks * BK;
       la.template issue_part<0, 1>(a_slot_s(ks), k0, a.K);
       if (CONV)
@@ -862,7 +910,26 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
   // i*2048 within the slot (likewise B with j).
   uint32_t va16[4], vb16[4];
   const int l16 = lane & 15, lq = lane >> 4;
-  if constexpr (PIPE == 3) {
+  // [K, N] B (PIPE 4): B fragment j of step t (k = 32t + 8lq .. +7, column
+  // colbase + 16j + l16) is two transposing reads of four k-rows each: in a
+  // 16-lane group, lane l16 addresses row 8lq + (l16 >> 2) (+4 for the second
+  // read), columns 16j + 4 (l16 & 3) .. +3, and receives column 16j + l16 of
+  // the four rows.  The row's swizzle term g depends on the lane alone
+  // (row & 3 = l16 >> 2, (row >> 3) & 1 = lq & 1); the LDS byte address per
+  // (slot, j), the step and the second read as immediate offsets.
+  uint32_t vbk[2][8];
+  if constexpr (PIPE == 4) {
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
+    const int g = (l16 >> 2) | ((lq & 1) << 2);
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        vbk[sb][j] = lds0 + (uint32_t)(sb ? 131072 : 32768) +
+                     (uint32_t)((8 * lq + (l16 >> 2)) * 512 +
+                                (colbase / 8 + 2 * (j ^ g) + ((l16 & 3) >> 1)) * 16 + (l16 & 1) * 8);
+  }
+  if constexpr (PIPE >= 3) {
     const int X0 = swz<RB>(l16);
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
@@ -876,7 +943,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     const int rows_it = subt ? SR : BM;
     f32x16 acc[4][NJ];
     f32x4 acc16[8][8];   // the four-wave form's 16 x 16 tiles
-    if constexpr (PIPE == 3) {
+    if constexpr (PIPE >= 3) {
 #pragma unroll
       for (int i = 0; i < 8; ++i)
 #pragma unroll
@@ -890,7 +957,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
           for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     }
 
-    if constexpr (PIPE == 3) {
+    if constexpr (PIPE >= 3) {
       // Four waves, one per SIMD, each a 128 x 128 quarter of the tile (8 x 8
       // tiles of 16 x 16); K a multiple of the 64-deep stage, taken as two
       // 32-deep steps of 64 MFMAs.  A of stage ks sits in slot ks % 3, B in
@@ -902,9 +969,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       // is a constant: no address arithmetic per fragment read, no K-bound
       // select per load (stages past the last read zeros via the stage
       // offset).
-      auto soff3 = [&](int ks, uint32_t range) __attribute__((always_inline)) -> uint32_t {
-        return ks < nk ? (uint32_t)ks * RB : range;
-      };
+      auto soff3 = [&](int ks, uint32_t range, uint32_t kstep) __attribute__((always_inline))
+          -> uint32_t { return ks < nk ? (uint32_t)ks * kstep : range; };
+      uint32_t kstep_b = RB;   // B's stage step along K ([K, N]: 64 rows)
+      if constexpr (PIPE == 4) kstep_b = lb.kstep;
       struct F16 {
         bf16x8 a[8], b[8];
       };
@@ -914,7 +982,27 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       };
       auto rd_b = [&](auto SB_, auto T_, int j, bf16x8& d) __attribute__((always_inline)) {
         constexpr int SB = decltype(SB_)::value, TT = decltype(T_)::value;
-        d = *(const bf16x8*)(smem + kSlotB3[SB] + j * 2048 + vb16[(2 * TT) ^ (j & 3)]);
+        if constexpr (PIPE == 4) {
+          // (asm: the compiler would wait for every direct-to-LDS load in
+          // flight before a transposing read; its results are waited for and
+          // redefined at the stage barrier and the stage end)
+          u32x2 lo, hi;
+          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                       : "=v"(lo) : "v"(vbk[SB == 0 ? 0 : 1][j]), "i"(TT * 16384));
+          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                       : "=v"(hi) : "v"(vbk[SB == 0 ? 0 : 1][j]), "i"(TT * 16384 + 2048));
+          d = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3));
+        } else {
+          d = *(const bf16x8*)(smem + kSlotB3[SB] + j * 2048 + vb16[(2 * TT) ^ (j & 3)]);
+        }
+      };
+      // The transposing reads' results exist after an LDS wait only: redefine
+      // them there so that no use is placed before it.
+      auto pin_b = [&](F16& f) __attribute__((always_inline)) {
+        if constexpr (PIPE == 4) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) asm volatile("" : "+v"(f.b[j]));
+        }
       };
       // One 32-deep step: 64 MFMAs on `cur`, row by row (A fragment i with
       // the 8 B fragments), in program order with the reads of the next
@@ -951,7 +1039,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
                       SA2 = (S6 + 2) % 3;
         using I0 = std::integral_constant<int, 0>;
         using I1 = std::integral_constant<int, 1>;
-        const uint32_t sa2 = soff3(ks + 2, la.range), sb2 = soff3(ks + 2, lb.range);
+        const uint32_t sa2 = soff3(ks + 2, la.range, RB), sb2 = soff3(ks + 2, lb.range, kstep_b);
         // step 0: reads of step 1, A(ks+2) into the slot stage ks-1 held
         step16(f0, f1, std::integral_constant<int, SA>{}, std::integral_constant<int, SB>{}, I1{},
                [&](int q) __attribute__((always_inline)) {
@@ -963,18 +1051,23 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
         __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
+        pin_b(f1);
         // step 1: reads of stage ks+1's step 0, B(ks+2) into B slot ks % 2
         step16(f1, f0, std::integral_constant<int, SA1>{}, std::integral_constant<int, SB1>{},
                I0{}, [&](int q) __attribute__((always_inline)) {
                  lb.issue_q(smem + kSlotB3[SB], sb2, q);
                });
+        if constexpr (PIPE == 4) {
+          __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): next stage's B fragments
+          pin_b(f0);
+        }
       };
       if (!staged0) {
         la.template issue_full<0, LA>(smem + kSlotA3[0], 0u);
         lb.template issue_full<0, LB>(smem + kSlotB3[0], 0u);
       }
-      la.template issue_full<0, LA>(smem + kSlotA3[1], soff3(1, la.range));
-      lb.template issue_full<0, LB>(smem + kSlotB3[1], soff3(1, lb.range));
+      la.template issue_full<0, LA>(smem + kSlotA3[1], soff3(1, la.range, RB));
+      lb.template issue_full<0, LB>(smem + kSlotB3[1], soff3(1, lb.range, kstep_b));
       if (staged0)
         wait_vm<LA + LB + kEpiVmem>();
       else
@@ -986,6 +1079,10 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
 #pragma unroll
       for (int i = 0; i < 8; ++i)
         rd_a(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{}, i, f0.a[i]);
+      if constexpr (PIPE == 4) {
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        pin_b(f0);
+      }
       int ks = 0;
       for (; ks + 6 <= nk; ks += 6) {
         stage3(std::integral_constant<int, 0>{}, ks);
@@ -1160,7 +1257,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     if (PIPE && more) {
       it_next = item_of(vn);
       init_loaders(it_next);
-      if constexpr (PIPE == 3) {
+      if constexpr (PIPE >= 3) {
         la.template issue_full<0, LA>(smem + kSlotA3[0], 0u);
         lb.template issue_full<0, LB>(smem + kSlotB3[0], 0u);
       } else if (CONV && it_next.sub >= 0) {
@@ -1188,7 +1285,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
     // the accumulators, in either MFMA layout.
     auto stage_any = [&](auto I_, auto J0_, float* sl) __attribute__((always_inline)) {
       constexpr int I = decltype(I_)::value, J0 = decltype(J0_)::value;
-      if constexpr (PIPE == 3)
+      if constexpr (PIPE >= 3)
         stage_slab16<I, J0>(acc16, sl, lqe, l16e);
       else
         stage_slab<I, NJ, J0>(acc, sl, lh, lr);
@@ -1434,7 +1531,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       gap_from_acc<T, NJ, SIG == kSigConvBiasReluGap>(a, acc, m0, n0, rowbase, colbase, wn, lr, lh,
                                                        pre_ch, rbias, red,
                                                        subt ? (rowbase < SR ? 1 : 0) : 4);
-    } else if (PIPE == 3 && m0 + BM <= a.M && n0 + BN <= a.N && vec_ok) {
+    } else if (PIPE >= 3 && m0 + BM <= a.M && n0 + BN <= a.N && vec_ok) {
       // Four-wave form, whole tile: the 8 passes (32-row slab I, 64-column
       // half H) alternate between the wave's two slabs; a pass reads its
       // slab back and then stages the next pass into the other one, so the
@@ -1447,7 +1544,7 @@ __global__ __launch_bounds__(128 * WN, (BN == 128 ? 2 : 1)) void gemm_mfma_kerne
       // row; residual pieces are requested two passes ahead.  The passes
       // exist twice, with and without the alpha multiply (alpha is 1 in most
       // modules: one VALU operation per value less).
-      if constexpr (PIPE == 3) {
+      if constexpr (PIPE >= 3) {
         const float alpha = a.alpha;
         const uint32_t ldc2 = (uint32_t)a.ldc * 2u;
         const uint32_t base0 =
@@ -1816,6 +1913,25 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
                        dim3(512), 0, st, a);
   } else {
     const int sig = gemm_signature(a);
+    if (four_wave_form(a, sig) && a.layout == 1) {
+      if constexpr (sizeof(T) == 2) {
+        switch (sig) {
+#define MK_GEMM_SIG4KN(SIG)                                                                   \
+  case SIG:                                                                                   \
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, 2, kGemmTileN, 2, 0, 4, 128, SIG>), grid, dim3(256), \
+                       0, st, a);                                                             \
+    break;
+          MK_GEMM_SIG4KN(kSigNone)
+          MK_GEMM_SIG4KN(kSigGeluErf)
+          MK_GEMM_SIG4KN(kSigAdd)
+          MK_GEMM_SIG4KN(kSigBias)
+          default:
+            MK_GEMM_SIG4KN(kSigBiasGeluTanhScale)
+#undef MK_GEMM_SIG4KN
+        }
+      }
+      return;
+    }
     if (four_wave_form(a, sig)) {
       switch (sig) {
 #define MK_GEMM_SIG4(SIG)                                                                     \
@@ -1852,6 +1968,14 @@ static void launch_gemm_t(const GemmArgs& a, dim3 grid, hipStream_t st) {
   }
 }
 
+// A [K, N] weight read in place by the four-wave form (no transpose): bf16,
+// one matrix, 256-wide tiles, K a multiple of the stage, a compiled chain.
+bool gemm_mfma_native_kn(int dtype, const GemmArgs& a) {
+  return dtype == MK_BF16 && a.layout == 1 && !a.conv && a.batch * a.heads == 1 &&
+         gemm_mfma_supported(dtype, a) && gemm_mfma_tile_n(dtype, a) == kGemmTileN &&
+         four_wave_form(a, gemm_signature(a));
+}
+
 int64_t gemm_mfma_tile_n(int dtype, const GemmArgs& a) {
   if (a.conv) return conv_wide(dtype, a) ? 256 : kConvTileN;
   const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + kGemmTileN - 1) / kGemmTileN) *
@@ -1866,7 +1990,7 @@ hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st) {
     if ((dtype != MK_BF16 && dtype != MK_F32) || a.cv_C % BKe || (a.cv_P * a.cv_Q) % 8 ||
         a.lda % E || a.K % BKe)
       return hipErrorInvalidValue;
-  } else if (!gemm_mfma_supported(dtype, a) || a.layout != 0) {
+  } else if (!gemm_mfma_supported(dtype, a) || (a.layout != 0 && !gemm_mfma_native_kn(dtype, a))) {
     return hipErrorInvalidValue;
   }
   if (((uintptr_t)a.A | (uintptr_t)a.B) % 16) return hipErrorInvalidValue;

@@ -150,6 +150,8 @@ hipError_t launch_gemm_mfma(int dtype, const GemmArgs& a, hipStream_t st);
 // terminal finishers follow it.
 constexpr int kSmallGemmTiles = 64;
 int64_t gemm_mfma_tile_n(int dtype, const GemmArgs& a);
+// True when a [K, N] weight (layout 1) is read in place, with no transpose.
+bool gemm_mfma_native_kn(int dtype, const GemmArgs& a);
 hipError_t launch_gemm_small(int dtype, const GemmArgs& a, hipStream_t st);
 // Implicit-GEMM conv: one packing launch (x -> zero-padded NHWC, w ->
 // [K][R][S][C]), the GEMM kernel in conv mode, and for a fused GAP the
